@@ -1,0 +1,194 @@
+/*
+ * chimera.h -- C ABI of an MI355X (gfx950) implementation of one Chimera
+ * decode step (Zeng et al., arXiv 2402.15758).
+ *
+ * One step is the paper's draft-then-verify iteration (Sec. 3.1, "Drafting"
+ * and "Verification"): the lightweight draft (Sec. 4.1: trigram encoder,
+ * Eq. 2; full-context encoder, Eq. 3; residual decoding heads, Eq. 4)
+ * proposes per-head top-k candidates that form a static token tree
+ * (Sec. 4.4); the target model scores the whole tree in one forward pass
+ * with tree-structured attention (Sec. 4.3); the longest path whose tokens
+ * equal the target's greedy choices is accepted (Sec. 4.3, greedy decoding)
+ * and its keys/values are compacted in place in the paged KV cache.
+ *
+ * Conventions for every call:
+ *  - All device memory is allocated by the caller (arena pointers) and only
+ *    borrowed by the library until the matching *_free call; the library
+ *    never frees caller memory.  Arena sizes come from the *_bytes queries.
+ *  - Streams are hipStream_t passed as void*; NULL means the null stream.
+ *  - Every call returns a chimera_status; nothing aborts or throws across the
+ *    ABI.  chimera_last_error() returns a thread-local message for the last
+ *    failure on the calling thread.
+ *  - Inputs are validated before any launch; on a validation error no state
+ *    changes.  An asynchronous HIP error surfaces as CHIMERA_EHIP at the
+ *    call's final synchronisation and poisons the context (later calls on it
+ *    return CHIMERA_ESTATE).
+ *  - A context is used by one host thread at a time.
+ */
+#ifndef CHIMERA_H
+#define CHIMERA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct chimera_model chimera_model; /* weights; read-only after load */
+typedef struct chimera_kv chimera_kv;       /* paged target KV + draft-encoder memory */
+typedef struct chimera_ctx chimera_ctx;     /* per-batch decode state and workspaces */
+
+typedef enum {
+  CHIMERA_OK = 0,
+  CHIMERA_EINVAL = -1,    /* bad argument, shape, token id or tree */
+  CHIMERA_ENOMEM = -2,    /* arena too small */
+  CHIMERA_ECAPACITY = -3, /* a sequence would outgrow its KV capacity */
+  CHIMERA_EHIP = -4,      /* a HIP runtime call or kernel failed */
+  CHIMERA_ESTATE = -5     /* context poisoned by an earlier HIP failure, or call out of order */
+} chimera_status;
+
+typedef enum { CHIMERA_F32 = 0, CHIMERA_BF16 = 1 } chimera_dtype;
+
+/* Shapes.  The target is a Llama-style decoder (the paper's backbones,
+ * Table 1): pre-RMSNorm blocks with multi-head attention and rotary
+ * positions (rotate-half pairs (i, i + head_dim/2), angle p * base^(-2i/hd)),
+ * SwiGLU feed-forward, final RMSNorm and an untied LM head.  The draft is the
+ * trigram MLP (Eq. 2), one encoder block of the same shape (Eq. 3) and
+ * n_draft_heads heads A_k (2d -> d), SiLU, Theta_k (d -> V) (Eq. 4). */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, n_draft_heads;
+  float rope_base; /* 10000 */
+  float rms_eps;   /* 1e-5 */
+  int32_t dtype;   /* chimera_dtype of weights and stored activations */
+  int32_t max_positions; /* size of the rotary tables: positions 0..max_positions-1 */
+} chimera_config;
+
+/* One weight tensor.  Names and shapes follow the canonical list:
+ *   tok_embed [V, d];
+ *   layers.{l}.{attn_norm [d], wq|wk|wv [d, H*hd], wo [H*hd, d], ffn_norm [d],
+ *               w_gate|w_up [d, F], w_down [F, d]};
+ *   final_norm [d]; lm_head [d, V];
+ *   draft.tri_w1 [3d, d]; draft.tri_w2 [d, d];
+ *   draft.enc.{same nine tensors as a layer};
+ *   draft.heads.{k}.a [2d, d]; draft.heads.{k}.theta [d, V].
+ * Matrices are row-major [d_in, d_out] (y = x @ W).  Norm gains are always
+ * float32; every other tensor has the config's dtype. */
+typedef struct {
+  const char* name;
+  const void* data;
+  int64_t numel;
+  int32_t dtype;     /* chimera_dtype */
+  int32_t on_device; /* 1: data is device memory, 0: host memory */
+} chimera_tensor;
+
+/* Bytes of the weight arena for this config (repacked weights + rotary
+ * tables). */
+chimera_status chimera_weight_bytes(const chimera_config* cfg, int64_t* bytes);
+
+/* Validate the tensor list and repack every tensor into `arena` (device
+ * memory of at least chimera_weight_bytes) in the order the GEMM kernels
+ * stream it.  Reads the caller's tensors once; they may be freed after the
+ * call returns.  Synchronises `stream`. */
+chimera_status chimera_load(const chimera_config* cfg, const chimera_tensor* tensors, int32_t n_tensors,
+                            void* arena, int64_t arena_bytes, void* stream, chimera_model** out);
+
+/* Paged target KV (page_size tokens per page, all layers, K and V) for up to
+ * max_batch sequences of at most max_len positions each, plus the draft
+ * encoder's memory.  n_pages must cover max_batch * ceil(max_len/page_size). */
+chimera_status chimera_kv_bytes(const chimera_model* m, int32_t max_batch, int32_t max_len, int32_t n_pages,
+                                int32_t page_size, int64_t* bytes);
+/* page_order (host, n_pages entries, nullable): the order in which physical
+ * pages are handed to sequences; NULL means 0, 1, 2, ... */
+chimera_status chimera_kv_create(chimera_model* m, int32_t max_batch, int32_t max_len, int32_t n_pages,
+                                 int32_t page_size, const int32_t* page_order, void* arena, int64_t arena_bytes,
+                                 chimera_kv** out);
+
+/* Decode context for a static candidate tree of n_nodes nodes (root
+ * included, n_nodes <= 64).  Node i has parent parent[i] (< i; -1 for the
+ * root, node 0) and takes the rank[i]-th candidate (rank < 8) of draft head
+ * depth(i)-1; siblings must have distinct ranks and depth(i) <=
+ * n_draft_heads.  n_nodes == 1 gives plain greedy autoregressive decoding
+ * (no draft). */
+chimera_status chimera_ctx_bytes(const chimera_model* m, const chimera_kv* kv, int32_t n_nodes, int64_t* bytes);
+chimera_status chimera_ctx_create(chimera_model* m, chimera_kv* kv, const int32_t* parent, const int32_t* rank,
+                                  int32_t n_nodes, void* arena, int64_t arena_bytes, chimera_ctx** out);
+
+/* Prefill (the prefix X, Sec. 4.1.1): run the target over each prompt,
+ * fill its KV pages and the draft encoder's memory, and return the first
+ * generated token of every sequence.  tokens (host) holds the prompts
+ * back to back; lens (host) their lengths (>= 1); batch <= max_batch.
+ * Synchronises `stream`. */
+chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, const int32_t* tokens,
+                               const int32_t* lens, int32_t batch, int32_t* first_tokens, void* stream);
+
+/* One draft -> verify -> accept -> compact iteration for every sequence.
+ * Outputs (host): new_tokens [batch][K+1] -- the accepted draft tokens in
+ * depth order followed by the bonus token (the target's argmax after the
+ * accepted path); n_new [batch] -- their count L, 1 <= L <= K+1; path_nodes
+ * [batch][K+1] (nullable) -- the accepted tree node ids from the root in
+ * depth order (L entries), i.e. the tree KV slots that were compacted.  The
+ * generated stream is the prefill token followed by every step's
+ * new_tokens; with greedy verification it equals greedy autoregressive
+ * decoding.  K = tree depth.  Synchronises `stream`. */
+chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, int32_t* new_tokens,
+                            int32_t* n_new, int32_t* path_nodes, void* stream);
+
+/* ---- benchmarking and parity hooks --------------------------------------
+ * Forced acceptance (synthetic workloads): at draft level k of a step with
+ * committed length n the predicted position is j = n+1+k; if ok[b*stride+j]
+ * the level's candidate list becomes ref[b*stride+j] followed by the best
+ * remaining ids, otherwise the best ids excluding ref[b*stride+j].  ref and
+ * ok are caller-owned device arrays [batch][stride] that must stay valid
+ * while forcing is set.  ref == NULL disables forcing. */
+chimera_status chimera_set_forcing(chimera_ctx* ctx, const int32_t* ref, const uint8_t* ok, int32_t stride);
+
+/* Replace the draft's tree tokens for nodes 1..n_nodes-1 of the next step
+ * only (host array [batch][n_nodes-1]); the root stays the pending token. */
+chimera_status chimera_set_tree_tokens(chimera_ctx* ctx, const int32_t* tokens, int32_t batch);
+
+enum {
+  CHIMERA_DBG_VERIFY_LOGITS = 0, /* float32 [batch*n_nodes][V], last step */
+  CHIMERA_DBG_DRAFT_LOGITS = 1,  /* float32 [batch][K][V], last step */
+  CHIMERA_DBG_TREE_TOKENS = 2,   /* int32 [batch][n_nodes], last step */
+  CHIMERA_DBG_DRAFT_LISTS = 3,   /* int32 [batch][K][8], last step's per-head lists */
+  CHIMERA_DBG_SEQ_LEN = 4,       /* int32 [batch], committed length n */
+  CHIMERA_DBG_TOKENS = 5         /* int32 [batch][max_len + 8], committed tokens then pending */
+};
+/* Copy a debug buffer to host memory (bytes must equal its size). */
+chimera_status chimera_debug_copy(chimera_ctx* ctx, int32_t what, void* dst, int64_t bytes);
+
+/* Read the target K and V of `count` positions starting at pos0 of
+ * sequence b in layer `layer` through the page table, into host arrays
+ * [count][H][hd] of the model dtype. */
+chimera_status chimera_kv_read(chimera_kv* kv, int32_t layer, int32_t b, int32_t pos0, int32_t count, void* k_out,
+                               void* v_out);
+
+/* Per-phase timing of steps, recorded with HIP events on the step's stream
+ * while enabled: draft, verify (tree pass + LM head), tail (accept, compact,
+ * advance) and the verify-pass GEMM launches alone. */
+typedef struct {
+  int64_t steps;
+  double ms_draft, ms_verify, ms_tail, ms_gemm_verify;
+  int64_t gemm_verify_launches;
+  double gemm_verify_bytes; /* algorithmic bytes of those launches: weights + activations in/out */
+  double verify_bytes;      /* algorithmic bytes of the verify passes: weights, KV read and write */
+} chimera_profile;
+chimera_status chimera_profile_enable(chimera_ctx* ctx, int32_t enable);
+chimera_status chimera_profile_read(chimera_ctx* ctx, chimera_profile* out);
+
+/* Test hook: y[M][N] (float32, host) = x[M][K] @ w[K][N] through the
+ * repack and GEMM kernels of `dtype`, on device buffers the call allocates
+ * and frees itself.  x and w are host arrays of that dtype. */
+chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
+                                  float* y);
+
+const char* chimera_last_error(void);
+void chimera_ctx_free(chimera_ctx* ctx);
+void chimera_kv_free(chimera_kv* kv);
+void chimera_free(chimera_model* m);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CHIMERA_H */

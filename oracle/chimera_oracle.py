@@ -335,7 +335,8 @@ class Forcing:
     """Forced-acceptance bias: at draft level k the predicted position is
     j = n + 1 + k.  If ok[j], the level list becomes [g_j] + the top-(s-1)
     of the rest; otherwise the top-s excluding g_j.  ``g`` and ``ok`` are
-    indexed by absolute position."""
+    indexed by absolute position; a negative g_j means no reference there
+    (plain top-s)."""
 
     def __init__(self, g: np.ndarray, ok: np.ndarray):
         self.g = np.asarray(g)
@@ -409,6 +410,8 @@ class Decoder:
         if f is None:
             return top_s(z, s)
         gj = int(f.g[j])
+        if gj < 0 or gj >= z.shape[0]:
+            return top_s(z, s)  # no reference token at this position: no bias
         if f.ok[j]:
             return [gj] + top_s(z, s - 1, exclude=gj)
         return top_s(z, s, exclude=gj)

@@ -1,0 +1,79 @@
+// Device helpers shared by the gfx950 kernels: storage types, rounding,
+// 16-byte fragments, MFMA on one k-block, and wave64 reductions.
+//
+// Every kernel is compiled with -ffp-contract=off: the arithmetic of a row
+// never depends on how many rows a launch carries or on which template
+// instance runs it, so a tree pass and a one-token pass produce identical
+// bits for the same logical inputs.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define CH_INF __builtin_inff()
+
+__device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
+
+// float -> bf16, round to nearest, ties to even (NaN -> quiet NaN).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// Storage-type traits.  A "fragment" is the 16 bytes one lane feeds into a
+// 16x16 MFMA k-block: VEC consecutive elements along the reduction axis.
+template <typename T> struct ET;
+template <> struct ET<float> {
+  static constexpr int VEC = 4;
+  __device__ static float to_f(float v) { return v; }
+  __device__ static float from_f(float v) { return v; }
+};
+template <> struct ET<bf16_t> {
+  static constexpr int VEC = 8;
+  __device__ static float to_f(bf16_t v) { return bf2f(v); }
+  __device__ static bf16_t from_f(float v) { return f2bf(v); }
+};
+
+__device__ __forceinline__ int4 ld16(const void* p) { return *reinterpret_cast<const int4*>(p); }
+__device__ __forceinline__ void st16(void* p, int4 v) { *reinterpret_cast<int4*>(p) = v; }
+
+// acc += A_frag x B_frag over one k-block of 4*VEC reduction indices.
+// Lane l supplies row/column (l & 15) and reduction indices (l >> 4)*VEC ..
+// +VEC-1 of the block.  bf16: one v_mfma_f32_16x16x32_bf16.  f32: four
+// v_mfma_f32_16x16x4_f32, the i-th consuming element i of every lane.
+template <typename T> __device__ __forceinline__ f32x4 mfma_kb(int4 a, int4 b, f32x4 acc);
+template <> __device__ __forceinline__ f32x4 mfma_kb<bf16_t>(int4 a, int4 b, f32x4 acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc,
+                                                 0, 0, 0);
+}
+template <> __device__ __forceinline__ f32x4 mfma_kb<float>(int4 a, int4 b, f32x4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(a.x), __int_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(a.y), __int_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(a.z), __int_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(a.w), __int_as_float(b.w), acc, 0, 0, 0);
+  return acc;
+}
+
+// Butterfly all-reductions over the 64 lanes of a wave.  Each stage adds a
+// lane's value to its partner's in commutative pairs, so every lane ends
+// with bit-identical results.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = v + __shfl_xor(v, m);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
+  return v;
+}
+
+__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
+
+// exp(a - b) for the online softmax, with exp(-inf - x) = 0.
+__device__ __forceinline__ float exp_diff(float a, float b) { return (a == -CH_INF) ? 0.0f : expf(a - b); }

@@ -1,0 +1,170 @@
+// Launch interface of the gfx950 kernels used by the host engine.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+enum { DT_F32 = 0, DT_BF16 = 1 };
+
+// ---- GEMM ------------------------------------------------------------------
+// Y = X[M][K] @ W[K][N] with W repacked into 1 KiB tiles: tile (nb, kb) holds
+// columns [16 nb, 16 nb + 16) and reduction indices [kb KB, kb KB + KB),
+// KB = 4 * VEC (32 for bf16, 16 for f32); lane l's 16 bytes are
+// W[kb KB + (l >> 4) VEC + e][16 nb + (l & 15)], e < VEC.  Tiles of one
+// column block are contiguous along kb, so a workgroup streams them linearly.
+enum { PACK_NATURAL = 0, PACK_QKV = 1, PACK_GU = 2 };
+// PACK_QKV interleaves, per head, the two halves of each rotary pair so that
+// packed column blocks 2p and 2p+1 hold dims [16p', 16p'+16) and
+// [hd/2 + 16p', ...) of the same head (V keeps its natural order);
+// PACK_GU interleaves gate and up: blocks 2p / 2p+1 = gate / up columns
+// [16p, 16p+16).
+
+enum { EPI_F32 = 0, EPI_T = 1, EPI_SILU = 2, EPI_SWIGLU = 3, EPI_QKV = 4, EPI_PARTIAL = 5 };
+
+struct GemmEpi {
+  int kind = EPI_F32;
+  float* out_f = nullptr;  // EPI_F32: [M][ldo]
+  void* out_t = nullptr;   // EPI_T / EPI_SILU / EPI_SWIGLU: [M][ldo] of the storage type
+  int ldo = 0;
+  float* part = nullptr;   // EPI_PARTIAL: [splits][M][N] (packed column order)
+  // EPI_QKV: per-row rotary position, KV element offset (-1: skip) and
+  // Q output row (-1: skip); K/V go to kbase/vbase + kvoff + h*head_stride.
+  const int* pos = nullptr;
+  const int64_t* kvoff = nullptr;
+  const int* qrow = nullptr;
+  void* kbase = nullptr;
+  void* vbase = nullptr;
+  int64_t head_stride = 0;
+  void* qout = nullptr;
+  int ldq = 0;
+  const float* rcos = nullptr;  // [max_pos][hd/2]
+  const float* rsin = nullptr;
+  int H = 0, hd = 0;
+};
+
+struct GemmShape {
+  const void* X = nullptr;
+  int ldx = 0;
+  int M = 0;
+  const void* W = nullptr;  // packed
+  int N = 0;                // packed columns of the whole matrix
+  int K = 0;
+  int nb_off = 0;           // first 16-column block to compute (even)
+  int nb_count = 0;         // number of 16-column blocks to compute (even); 0 = all
+  int splits = 1;           // split of the reduction across workgroups
+};
+
+// Splits chosen from (N, K) only, never from M.
+int gemm_pick_splits(int n_cols, int K, int dtype);
+void launch_gemm(int dtype, const GemmShape& s, const GemmEpi& e, float* scratch, hipStream_t st);
+void launch_repack(int dtype, int kind, const void* src0, const void* src1, const void* src2, int K, int n_src,
+                   void* dst, int H, int hd, hipStream_t st);
+
+// ---- elementwise / norms ------------------------------------------------------
+void launch_embed(int dtype, const int* tokens, const void* E, float* x, int M, int d, int V, hipStream_t st);
+// x[r] += sum_s parts[s][r] (if parts), optionally written back; out[r] =
+// T(rmsnorm(x[r]) * gamma).  Rows r in [alt_begin, alt_end) read their input
+// from alt[(r - alt_begin)] (storage type) instead of x.
+void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo,
+                    int M, int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end,
+                    hipStream_t st);
+
+// ---- attention ---------------------------------------------------------------
+struct TreeAttnArgs {
+  const void* q;            // [B*N][ldq] rotated queries
+  int ldq;
+  const void* kpool;        // layer base of K in the paged pool
+  const void* vpool;        // layer base of V
+  int64_t page_stride;      // elements between consecutive pages
+  const int* page_table;    // [B][max_pages]
+  int max_pages;
+  const int* n_b;           // [B] committed length
+  const int* depth;         // [N]
+  const uint8_t* path;      // [N][64]: node at each depth on the root->u path
+  int N, H, hd, ps, D;      // D = deepest node depth of the tree
+  float scale;
+  float* part_o;            // [B][H][G][N][hd]
+  float* part_ml;           // [B][H][G][N][2]
+  int G;                    // group slots (chunk groups of 8 x 64 positions)
+  void* out;                // [B*N][ldo]
+  int ldo;
+  int B;
+};
+void launch_tree_attn(int dtype, const TreeAttnArgs& a, hipStream_t st);
+
+struct EncAttnArgs {
+  const void* q;            // [B][ldq]
+  int ldq;
+  const void* kbase;        // encoder memory K [B][2][H][cap][hd]
+  const void* vbase;
+  int cap;
+  const int* n_b;           // [B]
+  int step;                 // chain step k: query at trigram position n + k
+  int H, hd;
+  float scale;
+  float* part;              // [B][H][nblk][hd + 2]
+  int nblk;
+  void* out;                // [B][ldo]
+  int ldo;
+  int B;
+};
+void launch_enc_attn(int dtype, const EncAttnArgs& a, hipStream_t st);
+
+// ---- decode-state kernels ------------------------------------------------------
+struct StepState {
+  int B, N, K, d, V, H, hd, ps, max_pages, tok_stride, cap;
+  int64_t page_stride;      // elements between pages in the target pool
+  int* n;                   // [B]
+  int* tok;                 // [B][tok_stride]: committed tokens, pending, chain tokens
+  void* h_last;             // [B][d]
+  const int* page_table;    // [B][max_pages]
+  const int* t_parent;      // [N]
+  const int* t_depth;       // [N]
+  const int* t_rank;        // [N]
+  const unsigned long long* t_anc;  // [N]
+  int* s_k;                 // [K] candidates per head
+  int* cand;                // [B][K][8]
+  int* tree_tok;            // [B*N]
+  const int* inject;        // [B][N-1] injected tree tokens
+  int* inject_on;           // [1]
+  const int* f_ref;         // forcing reference [B][f_stride] (nullable)
+  const uint8_t* f_ok;
+  int f_stride;
+  int* out_tok;             // [B][K+1]
+  int* out_nodes;           // [B][K+1]
+  int* out_len;             // [B]
+  int* pro_base;            // [B]
+  int* pro_count;           // [B]
+  void* pro_h;              // [B][K+1][d]
+  const void* hl;           // [B*N][d] post-final-norm verify states
+  const int* amax;          // [B*N]
+  // verify row descriptors
+  int* v_pos;               // [B*N]
+  int64_t* v_kvoff;         // [B*N]
+  int* v_qrow;              // [B*N]
+};
+void launch_argmax(const float* logits, int M, int V, int* amax, hipStream_t st);
+void launch_topk(const float* logits, const StepState& s, int level, hipStream_t st);
+void launch_tree_setup(const StepState& s, hipStream_t st);
+void launch_accept(int dtype, const StepState& s, hipStream_t st);
+void launch_compact(int dtype, const StepState& s, void* pool, int n_layers, int64_t layer_stride, hipStream_t st);
+void launch_advance(int dtype, const StepState& s, hipStream_t st);
+
+// Draft rows of chain step `level`.  Rows [0, B) are the chain queries
+// (trigram position n + level).  At level 0 rows [B, B + B(K+1)) are the
+// previous step's committed target-state entries and rows
+// [B + B(K+1), B + 2B(K+1)) their trigram entries.  Writes the trigram
+// inputs [rows][3d], rotary positions, encoder-memory offsets and Q rows.
+void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int* pos,
+                       int64_t* kvoff, int* qrow, hipStream_t st);
+// zin[b] = [h_last[b]; T(x[b] + sum_s parts[s][b])]
+void launch_draft_finish(int dtype, const StepState& s, const float* x, const float* parts, int n_parts, void* zin,
+                         hipStream_t st);
+// Prefill chunk rows: positions p0 .. p0+M-1 of sequence b; writes verify
+// descriptors (pos, kvoff through the page table, qrow), the token list,
+// trigram inputs for the same positions and the encoder descriptors of the
+// target-state rows [0, M) and trigram rows [M, 2M).
+void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, int p0, int M, int* tokens_out,
+                         void* tri_in, int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n, hipStream_t st);
+// Prefill end: pending token, h_last, committed length and tokens.
+void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,
+                           hipStream_t st);

@@ -1,0 +1,95 @@
+"""Shared pieces of the GPU parity tests: sessions built from the synthetic
+workloads, and a teacher-forced comparison of one GPU step with the oracle.
+
+Parity rule (numeric contract): verify logits within tau * (max - min) of the
+oracle's per node (tau = 1e-4 for f32 models, 2e-2 for bf16); tokens, tree
+node ids and the accepted path bit-exact.  For bf16 models a differing
+argmax or top-s choice is admissible only when the oracle's own margin
+between the two ids is <= 2 tau * range; such ties are counted and the
+oracle then follows the GPU's choice.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+import synth
+from oracle import chimera_oracle as co
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def tau(cfg):
+    return 2e-2 if cfg.dtype == "bf16" else 1e-4
+
+
+def make_session(cfg, weights, tree, max_batch=1, max_len=512, page_order=None):
+    from paper_2402_15758_amd import Session
+    return Session(cfg, weights, tree, max_batch=max_batch, max_len=max_len, page_order=page_order)
+
+
+class TieLog:
+    def __init__(self):
+        self.argmax_ties = 0
+        self.list_ties = 0
+
+
+def compare_lists(gpu_list, o_list, z, t, ties: TieLog, forced_first: bool):
+    """Compare a GPU top-s list with the oracle's for one draft head."""
+    if list(gpu_list) == list(o_list):
+        return
+    rng = float(z.max() - z.min())
+    for r, (a, b) in enumerate(zip(gpu_list, o_list)):
+        if a == b:
+            continue
+        assert not (forced_first and r == 0), "forced rank-0 token differs"
+        assert abs(float(z[a]) - float(z[b])) <= 2 * t * rng, (
+            f"draft rank {r}: gpu {a} vs oracle {b}, margin {abs(z[a] - z[b]):.3g} > {2 * t * rng:.3g}")
+        ties.list_ties += 1
+
+
+def gpu_step(sess):
+    """One GPU step plus the debug buffers the comparison needs."""
+    from paper_2402_15758_amd import binding as B
+    toks, n, path = sess.step()
+    art = dict(toks=toks, n=n, path=path, tree=sess.debug(B.DBG_TREE_TOKENS),
+               logits=sess.debug(B.DBG_VERIFY_LOGITS).reshape(sess.batch, sess.n_nodes, -1))
+    if sess.K:
+        art["lists"] = sess.debug(B.DBG_DRAFT_LISTS)
+    return art
+
+
+def check_step(art, b: int, dec: oracle.Decoder, t: float, ties: TieLog, forced=None):
+    """Check sequence b of a GPU step against the oracle driven along the
+    GPU's state; the oracle then commits what the GPU committed."""
+    L = int(art["n"][b])
+    tree_g = art["tree"][b]
+    logits_g = art["logits"][b]
+    if dec.K:
+        lists_o, dz = dec.draft()
+        for k in range(dec.K):
+            ff = forced is not None and bool(forced.ok[dec.n + 1 + k])
+            compare_lists(art["lists"][b, k, : dec.s[k]], lists_o[k], dz[k], t, ties, ff)
+    assert int(tree_g[0]) == dec.pending
+    logits_o, h_o, tkv = dec.verify(list(tree_g))
+    rngs = logits_o.max(-1) - logits_o.min(-1)
+    err = float(np.max(np.abs(logits_g - logits_o) / rngs[:, None]))
+    assert err <= t, f"verify logits rel err {err:.3g} > {t}"
+    amax_g = logits_g.argmax(-1)
+    amax_o = logits_o.argmax(-1)
+    for u in range(len(tree_g)):
+        if amax_g[u] != amax_o[u]:
+            z = logits_o[u]
+            assert abs(z[amax_g[u]] - z[amax_o[u]]) <= 2 * t * rngs[u], f"node {u} argmax differs beyond tie"
+            ties.argmax_ties += 1
+    path_o, bonus_o = dec.accept(list(tree_g), list(amax_g))
+    assert list(art["path"][b, :L]) == path_o, (list(art["path"][b, :L]), path_o)
+    new_o = [int(tree_g[u]) for u in path_o[1:]] + [int(bonus_o)]
+    assert list(art["toks"][b, :L]) == new_o
+    dec.commit(path_o, bonus_o, list(tree_g), h_o, tkv)
+    return new_o, err

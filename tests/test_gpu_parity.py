@@ -1,0 +1,276 @@
+"""GPU parity of the Chimera decode step against the CPU oracle, through the
+C ABI.  Each test prints the case it runs before touching the GPU."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_helpers import TieLog, check_step, gpu_step, log, make_session, tau
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------------------
+# GEMM unit (repack + MFMA GEMM), including row-count invariance
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 256), (8, 96, 512), (64, 4096, 4096), (100, 1024, 1536), (256, 128, 11008)])
+def test_gemm_matches_fp64(dtype, M, N, K):
+    import torch
+    from paper_2402_15758_amd import binding as B
+    if dtype == "f32" and K % 16:
+        pytest.skip("K must be a multiple of 16")
+    log(f"gemm {dtype} M={M} N={N} K={K}")
+    g = torch.Generator().manual_seed(M * 7 + N + K)
+    x = torch.randn(M, K, generator=g)
+    w = torch.randn(K, N, generator=g) * 0.05
+    if dtype == "bf16":
+        xt, wt = x.to(torch.bfloat16), w.to(torch.bfloat16)
+        x64, w64 = xt.double(), wt.double()
+        xb, wb = xt.view(torch.int16).numpy(), wt.view(torch.int16).numpy()
+        code = B.CHIMERA_BF16
+    else:
+        x64, w64 = x.double(), w.double()
+        xb, wb = x.numpy(), w.numpy()
+        code = B.CHIMERA_F32
+    y = np.zeros((M, N), dtype=np.float32)
+    B.chimera_debug_gemm(code, xb.ctypes.data, wb.ctypes.data, M, N, K, y.ctypes.data)
+    ref = (x64 @ w64).numpy()
+    bound = (x64.abs() @ w64.abs()).numpy()
+    assert np.all(np.abs(y - ref) <= 2e-5 * bound + 1e-30)
+    # one row alone gives the same bits as inside the M-row launch
+    r = M // 2
+    y1 = np.zeros((1, N), dtype=np.float32)
+    xr = np.ascontiguousarray(xb[r:r + 1])
+    B.chimera_debug_gemm(code, xr.ctypes.data, wb.ctypes.data, 1, N, K, y1.ctypes.data)
+    assert np.array_equal(y1[0].view(np.uint32), y[r].view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# Tiny fp32 workload: full independent runs, bit-exact tokens
+# ---------------------------------------------------------------------------
+@pytest.fixture(scope="module")
+def tiny():
+    cfg = synth.TINY
+    w = synth.make_weights(cfg, device="cpu")
+    orc = oracle.Oracle(cfg, synth.weights_to_numpy(w))
+    prompt = synth.WORKLOADS["tiny"].prompts()[0]
+    return cfg, w, orc, prompt
+
+
+def test_tiny_full_run_bitexact(tiny):
+    cfg, w, orc, prompt = tiny
+    log("tiny fp32: T8, 64 tokens, unforced")
+    sess = make_session(cfg, w, synth.TREE_T8, max_len=256)
+    first = sess.prefill([prompt])
+    dec = oracle.Decoder(orc, synth.TREE_T8)
+    assert int(first[0]) == dec.prefill(list(prompt))
+    ties = TieLog()
+    out, worst = [int(first[0])], 0.0
+    while len(out) < 64:
+        art = gpu_step(sess)
+        new, err = check_step(art, 0, dec, tau(cfg), ties)
+        out += new
+        worst = max(worst, err)
+    assert ties.argmax_ties == 0 and ties.list_ties == 0
+    assert out[:64] == orc.greedy_ar(list(prompt), 64)
+    log(f"tiny worst logit rel err {worst:.2e}")
+    sess.close()
+
+
+@pytest.mark.parametrize("std", [0.06])
+def test_tiny_varied_weights_spec_equals_ar(std):
+    cfg = synth.TINY
+    w = synth.make_weights(cfg, std=std, device="cpu")
+    orc = oracle.Oracle(cfg, synth.weights_to_numpy(w))
+    prompt = synth.make_prompt(45, cfg.vocab, 21)
+    log(f"tiny fp32 std={std}: spec vs AR, 48 tokens")
+    spec = make_session(cfg, w, synth.TREE_T8, max_len=256)
+    out_s, _ = spec.generate([prompt], 48)
+    ar = make_session(cfg, w, (), max_len=256)
+    out_a, steps = ar.generate([prompt], 48)
+    assert out_s[0] == out_a[0] == orc.greedy_ar(list(prompt), 48)
+    assert all(int(n[0]) == 1 for _, n, _ in steps)
+
+
+def test_tiny_forced_acceptance_closed_form(tiny):
+    import torch
+    cfg, w, orc, prompt = tiny
+    log("tiny fp32: forced p=0.7")
+    n0, G = len(prompt), 64
+    ar = orc.greedy_ar(list(prompt), G + 8)
+    max_len = 256
+    stride = max_len + 8
+    ref = np.full((1, stride), -1, dtype=np.int32)
+    ref[0, n0:n0 + len(ar)] = ar
+    ok = synth.force_table(0.7, 3, 0, stride)[None]
+    sess = make_session(cfg, w, synth.TREE_T8, max_len=max_len)
+    sess.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+    out, steps = sess.generate([prompt], G)
+    assert out[0] == ar[:G]
+    n = n0
+    for toks, nn, path in steps:
+        run = 0
+        while run < 3 and ok[0, n + 1 + run]:
+            run += 1
+        assert int(nn[0]) == 1 + run
+        n += int(nn[0])
+    # the oracle along the same forcing takes the same steps
+    dec = oracle.Decoder(orc, synth.TREE_T8, oracle.Forcing(ref[0], ok[0]))
+    out_o, steps_o = dec.generate(list(prompt), G)
+    assert out_o == out[0]
+    assert [a["path"] for a in steps_o] == [list(p[0, : int(nn[0])]) for _, nn, p in steps]
+
+
+def test_tiny_kv_compaction_equals_prefill(tiny):
+    cfg, w, orc, prompt = tiny
+    log("tiny fp32: KV contents after forced steps (shuffled pages)")
+    import torch
+    max_len = 256
+    stride = max_len + 8
+    n0 = len(prompt)
+    ar = orc.greedy_ar(list(prompt), 40)
+    ref = np.full((1, stride), -1, dtype=np.int32)
+    ref[0, n0:n0 + 40] = ar
+    ok = np.ones((1, stride), dtype=np.uint8)  # p = 1: every step accepts K + 1
+    n_pages = int(np.ceil((max_len + 64) / 16))
+    order = np.random.default_rng(0).permutation(n_pages).astype(np.int32)
+    sess = make_session(cfg, w, synth.TREE_T8, max_len=max_len, page_order=order)
+    sess.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+    sess.prefill([prompt])
+    for _ in range(5):
+        _, nn, path = sess.step()
+        assert int(nn[0]) == 4 and list(path[0]) == [0, 1, 4, 7]
+    n = int(sess.debug(4)[0])
+    seq = list(prompt) + ar[: n - n0]
+    _, _, kv = orc.causal_forward(seq)
+    for layer in range(cfg.n_layers):
+        k, v = sess.kv_read(layer, 0, 0, n)
+        np.testing.assert_allclose(k, kv[layer][0], rtol=1e-4, atol=1e-5)
+        np.testing.assert_allclose(v, kv[layer][1], rtol=1e-4, atol=1e-5)
+
+
+def test_tiny_injected_tree_tokens(tiny):
+    """Verify/accept/compact on oracle-chosen tree tokens (draft bypassed):
+    a tree whose rank-0 chain holds the greedy continuation accepts it."""
+    cfg, w, orc, prompt = tiny
+    log("tiny fp32: injected tree tokens")
+    sess = make_session(cfg, w, synth.TREE_T8, max_len=256)
+    dec = oracle.Decoder(orc, synth.TREE_T8)
+    sess.prefill([prompt])
+    dec.prefill(list(prompt))
+    rng = np.random.default_rng(5)
+    ties = TieLog()
+    for trial in range(4):
+        ar = orc.greedy_ar(dec.seq[: dec.n + 1], 3)
+        toks = rng.integers(0, cfg.vocab, 7).astype(np.int32)
+        if trial % 2 == 0:  # put the greedy chain on nodes 1, 4, 7
+            toks[0], toks[3], toks[6] = ar[0], ar[1], ar[2]
+        sess.set_tree_tokens(toks[None])
+        art = gpu_step(sess)
+        assert list(art["tree"][0, 1:]) == list(toks)
+        dz = dec.draft()  # keep the oracle's draft state in step
+        logits_o, h_o, tkv = dec.verify([dec.pending] + list(toks))
+        rngs = logits_o.max(-1) - logits_o.min(-1)
+        assert np.max(np.abs(art["logits"][0] - logits_o) / rngs[:, None]) <= tau(cfg)
+        path, bonus = dec.accept([dec.pending] + list(toks), list(logits_o.argmax(-1)))
+        L = int(art["n"][0])
+        assert list(art["path"][0, :L]) == path
+        if trial % 2 == 0:
+            assert path == [0, 1, 4, 7]
+        dec.commit(path, bonus, [dec.pending] + list(toks), h_o, tkv)
+
+
+# ---------------------------------------------------------------------------
+# Small bf16 model with the 7B head size: teacher-forced parity, spec == AR
+# ---------------------------------------------------------------------------
+SMALL = synth.small_config(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=512, vocab=2048,
+                           n_draft_heads=4)
+
+
+@pytest.fixture(scope="module")
+def small():
+    w = synth.make_weights(SMALL, std=0.06, device="cpu")
+    orc = oracle.Oracle(SMALL, synth.weights_to_numpy(w))
+    return w, orc
+
+
+@pytest.mark.parametrize("n0,tree", [(90, "T64"), (600, "T32"), (61, "T64")])
+def test_small_bf16_teacher_forced(small, n0, tree):
+    w, orc = small
+    log(f"small bf16: prompt {n0}, {tree}, teacher-forced steps")
+    ranks = synth.TREES[tree]
+    prompt = synth.make_prompt(n0, SMALL.vocab, 30 + n0)
+    sess = make_session(SMALL, w, ranks, max_len=1024)
+    first = sess.prefill([prompt])
+    dec = oracle.Decoder(orc, ranks)
+    f_o = dec.prefill(list(prompt))
+    assert int(first[0]) == f_o
+    ties = TieLog()
+    for _ in range(10):
+        check_step(gpu_step(sess), 0, dec, tau(SMALL), ties)
+    log(f"ties: argmax {ties.argmax_ties}, lists {ties.list_ties}")
+
+
+def test_small_bf16_spec_equals_ar_bitexact(small):
+    """GPU speculative decoding reproduces GPU greedy decoding token for
+    token: every kernel's per-row arithmetic is independent of the tree."""
+    import torch
+    w, _ = small
+    log("small bf16: GPU spec (forced p=0.7) vs GPU AR, 120 tokens")
+    prompt = synth.make_prompt(100, SMALL.vocab, 77)
+    G, max_len = 120, 512
+    ar_s = make_session(SMALL, w, (), max_len=max_len)
+    out_a, _ = ar_s.generate([prompt], G + 8)
+    stride = max_len + 8
+    ref = np.full((1, stride), -1, dtype=np.int32)
+    ref[0, 100:100 + G + 8] = out_a[0]
+    ok = synth.force_table(0.7, 3, 0, stride)[None]
+    sp = make_session(SMALL, w, synth.TREE_T64, max_len=max_len)
+    sp.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+    out_s, steps = sp.generate([prompt], G)
+    assert out_s[0] == out_a[0][:G]
+    n = 100
+    for toks, nn, path in steps:
+        run = 0
+        while run < 4 and ok[0, n + 1 + run]:
+            run += 1
+        assert int(nn[0]) == 1 + run
+        n += int(nn[0])
+
+
+def test_small_bf16_batch_ragged(small):
+    """Batch of 3 ragged sequences with different forcing rates; each
+    sequence equals its own greedy decoding and the oracle's parity holds."""
+    import torch
+    w, orc = small
+    log("small bf16: batch 3 ragged, T32")
+    lens = [70, 130, 200]
+    prompts = [synth.make_prompt(n, SMALL.vocab, 500 + n) for n in lens]
+    max_len, G = 512, 40
+    stride = max_len + 8
+    ar_s = make_session(SMALL, w, (), max_batch=3, max_len=max_len)
+    out_a, _ = ar_s.generate(prompts, G + 8)
+    ref = np.full((3, stride), -1, dtype=np.int32)
+    oks = []
+    for b, n in enumerate(lens):
+        ref[b, n:n + G + 8] = out_a[b]
+        oks.append(synth.force_table([0.4, 0.7, 0.9][b], 5, b, stride))
+    ok = np.stack(oks)
+    sp = make_session(SMALL, w, synth.TREE_T32, max_batch=3, max_len=max_len)
+    sp.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+    first = sp.prefill(prompts)
+    decs = []
+    for b in range(3):
+        d = oracle.Decoder(orc, synth.TREE_T32, oracle.Forcing(ref[b], ok[b]))
+        assert d.prefill(list(prompts[b])) == int(first[b])
+        decs.append(d)
+    ties = TieLog()
+    outs = [[int(f)] for f in first]
+    for _ in range(8):
+        art = gpu_step(sp)
+        for b in range(3):
+            new, _ = check_step(art, b, decs[b], tau(SMALL), ties, forced=decs[b].forcing)
+            outs[b] += new
+    for b in range(3):
+        assert outs[b] == out_a[b][: len(outs[b])]
