@@ -1,0 +1,250 @@
+"""Benchmark of the Chimera decode step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--no-cpu-baseline]
+
+A step is one chimera_step: draft chain, tree assembly, the target's verify
+pass over the whole candidate tree, greedy acceptance and KV compaction.
+The default workload is the Llama-7B-shaped bf16 model (random N(0, 0.02)
+weights), batch 1, a uniform random 512-token prompt, the 64-node tree and
+forced acceptance p = 0.7 (the paper's datasets and trained drafts are
+replaced by synthetic prompts and a seeded acceptance bias).  W untimed
+steps run first, then exactly K steps are timed; the line printed is
+
+  value = accepted (committed) tokens / timed seconds.
+
+Also reported: the verify GEMM kernel's achieved HBM bandwidth from HIP
+events around each of its launches in the timed steps (roofline), the whole
+verify pass's fraction of HBM peak, the plain greedy decoding rate of the
+same GPU path (tree of one node) and the CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=60)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama7b_p512")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ar", action="store_true", help="skip timing the greedy-decoding rate")
+    return ap.parse_args()
+
+
+def forcing_tables(wl, prompts, ar_streams, stride):
+    """Reference greedy stream and seeded success bits per sequence."""
+    import synth
+    B = len(prompts)
+    ref = np.full((B, stride), -1, dtype=np.int32)
+    ok = np.zeros((B, stride), dtype=np.uint8)
+    ps = wl.accept_probs()
+    for b in range(B):
+        n0 = len(prompts[b])
+        a = ar_streams[b][: stride - n0]
+        ref[b, n0:n0 + len(a)] = a
+        ok[b] = synth.force_table(ps[b], wl.force_seed, b, stride)
+    return ref, ok
+
+
+def cpu_baseline(wl, weights_gpu, prompt, accept_len):
+    """The oracle on a bounded sample of the workload: one decode step of
+    the full draft and of the first two target layers plus the LM head,
+    after a prefill of the same prompt; the target part is scaled to all
+    layers.  Reported in accepted tokens/s with the realised mean accepted
+    length of the GPU run."""
+    import dataclasses
+
+    import oracle
+    import synth
+    cfg = wl.model
+    n_sample = 2
+    sub = dataclasses.replace(cfg, n_layers=n_sample)
+    keep = [n for n, _, _ in synth.tensor_specs(sub)]
+    w = synth.weights_to_numpy({k: weights_gpu[k] for k in keep})
+    threads = len(os.sched_getaffinity(0))
+    omp = os.environ.get("OMP_NUM_THREADS")
+    if omp:
+        threads = min(threads, int(omp))
+    orc = oracle.Oracle(sub, w, compute=np.float32)
+    dec = oracle.Decoder(orc, synth.TREES[wl.tree])
+    t0 = time.perf_counter()
+    dec.prefill(list(prompt))
+    t_prefill = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    lists, _ = dec.draft()
+    t_draft = time.perf_counter() - t0
+    toks = dec.assemble(lists)
+    t0 = time.perf_counter()
+    logits, h, tkv = dec.verify(toks)
+    t_verify = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    _ = h @ orc.w("lm_head")
+    t_head = time.perf_counter() - t0
+    t_layers = max(t_verify - t_head, 0.0)
+    t_step = t_draft + t_layers * (cfg.n_layers / n_sample) + t_head
+    return {
+        "value": accept_len / t_step,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"one float32 oracle step (draft + {n_sample} of {cfg.n_layers} target layers + LM head, "
+                   f"64-node tree, context {len(prompt)}), target layers scaled x{cfg.n_layers // n_sample}; "
+                   f"prefill {t_prefill:.1f}s excluded; step {t_step:.2f}s"),
+    }
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(the decode step of one sequence batch lives on one MI355X)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import synth
+    from paper_2402_15758_amd import Session
+
+    wl = synth.WORKLOADS[a.workload]
+    cfg = wl.model
+    prompts = wl.prompts()
+    K_levels = max(len(r) for r in synth.TREES[wl.tree])
+    total_steps = a.warmup + a.steps
+    max_len = max(len(p) for p in prompts) + total_steps * (K_levels + 1) + 128
+    max_len = (max_len + 63) // 64 * 64
+    torch.cuda.init()
+    dev = torch.device("cuda:0")
+    log(f"[bench] workload {wl.name}: generating weights on the GPU")
+    t0 = time.perf_counter()
+    weights = synth.make_weights(cfg, wl.target_seed, wl.draft_seed, device="cuda")
+    torch.cuda.synchronize()
+    log(f"[bench] weights ready in {time.perf_counter() - t0:.1f}s; loading")
+    spec = Session(cfg, weights, synth.TREES[wl.tree], max_batch=len(prompts), max_len=max_len)
+    ar = Session(cfg, None, (), max_batch=len(prompts), max_len=max_len, share_model=spec)
+    torch.cuda.synchronize()
+
+    # greedy reference stream (plain decoding through the same kernels)
+    n_ref = total_steps * (K_levels + 1) + K_levels + 2
+    log(f"[bench] greedy decoding {n_ref} tokens for the forcing reference")
+    streams = [[int(t)] for t in ar.prefill(prompts)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while min(len(s) for s in streams) < n_ref:
+        toks, n, _ = ar.step()
+        for b in range(len(prompts)):
+            streams[b] += [int(x) for x in toks[b, : n[b]]]
+    torch.cuda.synchronize()
+    ar_rate = len(prompts) * (n_ref - 1) / (time.perf_counter() - t0)
+    stride = max_len + 8
+    ref, ok = forcing_tables(wl, prompts, streams, stride)
+    spec.set_forcing(torch.from_numpy(ref).to(dev), torch.from_numpy(ok).to(dev))
+
+    log(f"[bench] spec: prefill, {a.warmup} warmup steps, {a.steps} timed steps")
+    first = spec.prefill(prompts)
+    out = [[int(t)] for t in first]
+    for _ in range(a.warmup):
+        toks, n, _ = spec.step()
+        for b in range(len(prompts)):
+            out[b] += [int(x) for x in toks[b, : n[b]]]
+    spec.profile(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    accepted = 0
+    for _ in range(a.steps):
+        toks, n, _ = spec.step()
+        accepted += int(n.sum())
+        for b in range(len(prompts)):
+            out[b] += [int(x) for x in toks[b, : n[b]]]
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prof = spec.profile_read()
+    spec.profile(False)
+    lossless = all(out[b] == streams[b][: len(out[b])] for b in range(len(prompts)))
+    value = accepted / dt
+    gemm_gbs = prof.gemm_verify_bytes / (prof.ms_gemm_verify * 1e-3) / 1e9
+    verify_gbs = prof.verify_bytes / (prof.ms_verify * 1e-3) / 1e9
+    per_launch_bytes = prof.gemm_verify_bytes / max(prof.gemm_verify_launches, 1)
+    per_launch_us = prof.ms_gemm_verify * 1e3 / max(prof.gemm_verify_launches, 1)
+    log(f"[bench] {value:.1f} tok/s, {dt / a.steps * 1e3:.3f} ms/step, accept {accepted / a.steps / len(prompts):.3f}, "
+        f"verify {prof.ms_verify / prof.steps:.3f} ms ({verify_gbs:.0f} GB/s), draft {prof.ms_draft / prof.steps:.3f} ms, "
+        f"gemm {gemm_gbs:.0f} GB/s, lossless={lossless}")
+
+    cpu = None
+    if not a.no_cpu_baseline and len(prompts) == 1:
+        log("[bench] CPU oracle baseline (bounded sample)")
+        try:
+            cpu = cpu_baseline(wl, weights, prompts[0], accepted / a.steps)
+        except MemoryError:
+            cpu = None
+    line = {
+        "metric": "accepted tokens/sec at batch 1 (Llama-7B-shape bf16); verify-pass % of HBM peak",
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(dt / a.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "target": f"{cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} F{cfg.d_ffn} V{cfg.vocab}",
+            "draft": f"trigram MLP + 1 encoder layer + {cfg.n_draft_heads} heads",
+            "batch": len(prompts),
+            "prompt_len": [len(p) for p in prompts] if len(prompts) > 1 else len(prompts[0]),
+            "tree": wl.tree,
+            "accept_p": wl.accept_p[0] if wl.accept_p and len(prompts) == 1 else wl.accept_p,
+            "page_size": 16,
+        },
+        "roofline": {
+            "kernel": "verify GEMMs (QKV, O, gate/up, down, LM head)",
+            "bound": "hbm",
+            "achieved": round(gemm_gbs, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(gemm_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "bytes_per_launch": round(per_launch_bytes),
+            "us_per_launch": round(per_launch_us, 2),
+        },
+        "verify_pass": {
+            "ms": round(prof.ms_verify / prof.steps, 4),
+            "bytes": round(prof.verify_bytes / prof.steps),
+            "achieved_gbs": round(verify_gbs, 1),
+            "frac_hbm_peak": round(verify_gbs / HBM_PEAK_GBS, 4),
+        },
+        "draft_ms": round(prof.ms_draft / prof.steps, 4),
+        "tail_ms": round(prof.ms_tail / prof.steps, 4),
+        "accept_len_mean": round(accepted / a.steps / len(prompts), 4),
+        "lossless_vs_greedy": lossless,
+        "greedy_tokens_per_s": round(ar_rate, 2),
+        "speedup_vs_greedy": round(value / ar_rate, 3),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    spec.close()
+    ar.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -30,8 +30,9 @@ class Session:
     n_draft_heads, rope_base, rms_eps and dtype ("f32" | "bf16");
     ``weights`` maps the canonical tensor names to torch tensors."""
 
-    def __init__(self, cfg, weights: Dict[str, "object"], tree_ranks, max_batch: int = 1, max_len: int = 1024,
-                 page_size: int = 16, page_order: Optional[np.ndarray] = None, device: str = "cuda"):
+    def __init__(self, cfg, weights: Optional[Dict[str, "object"]], tree_ranks, max_batch: int = 1,
+                 max_len: int = 1024, page_size: int = 16, page_order: Optional[np.ndarray] = None,
+                 device: str = "cuda", share_model: Optional["Session"] = None):
         import torch
 
         self.torch = torch
@@ -42,17 +43,25 @@ class Session:
         c = B.chimera_config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ffn, cfg.vocab,
                              cfg.n_draft_heads, float(cfg.rope_base), float(cfg.rms_eps), self.dt, max_len + 128)
         self._c = c
-        wb = B.chimera_weight_bytes(c)
-        self.w_arena = torch.empty(wb, dtype=torch.uint8, device=self.device)
-        names, tensors = [], []
-        for name, t in weights.items():
-            t = t.contiguous()
-            nb = name.encode()
-            names.append((nb, t))
-            dt = B.CHIMERA_F32 if t.dtype == torch.float32 else B.CHIMERA_BF16
-            tensors.append(B.chimera_tensor(nb, t.data_ptr(), t.numel(), dt, 1 if t.is_cuda else 0))
-        self.model = B.chimera_load(c, tensors, self.w_arena.data_ptr(), wb, self.stream())
-        del names, tensors
+        self._owner = share_model is None
+        if share_model is not None:
+            # another decode state over the same loaded weights
+            if share_model.cfg != cfg or share_model.max_len < max_len:
+                raise ValueError("shared model has another config or a shorter rotary table")
+            self.w_arena, self.model = share_model.w_arena, share_model.model
+            self._c = share_model._c
+        else:
+            wb = B.chimera_weight_bytes(c)
+            self.w_arena = torch.empty(wb, dtype=torch.uint8, device=self.device)
+            names, tensors = [], []
+            for name, t in weights.items():
+                t = t.contiguous()
+                nb = name.encode()
+                names.append((nb, t))
+                dt = B.CHIMERA_F32 if t.dtype == torch.float32 else B.CHIMERA_BF16
+                tensors.append(B.chimera_tensor(nb, t.data_ptr(), t.numel(), dt, 1 if t.is_cuda else 0))
+            self.model = B.chimera_load(c, tensors, self.w_arena.data_ptr(), wb, self.stream())
+            del names, tensors
         self.page_size = page_size
         self.n_pages = max_batch * math.ceil((max_len + 64) / page_size)
         if page_order is not None:
@@ -158,7 +167,8 @@ class Session:
             B.chimera_kv_free(self.kv)
             self.kv = None
         if getattr(self, "model", None):
-            B.chimera_free(self.model)
+            if self._owner:
+                B.chimera_free(self.model)
             self.model = None
 
     def __del__(self):
