@@ -193,6 +193,8 @@ struct chimera_ctx {
   float* dlogits = nullptr;
   float* dparts = nullptr;
   float* enc_part = nullptr;
+  float* topk_v = nullptr;
+  int* topk_i = nullptr;
   // host side
   int batch = 0;
   std::vector<int> n_host;
@@ -503,7 +505,7 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
     et.out_f = c->dlogits + (size_t)k * V;
     et.ldo = K * V;
     g.run(c->ak, d, B, m->head_theta[k], V, d, et);
-    launch_topk(c->dlogits, s, k, st);
+    launch_topk(c->dlogits, s, k, c->topk_v, c->topk_i, st);
   }
 }
 
@@ -592,6 +594,8 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   c->dlogits = a.arr<float>(B * std::max<size_t>(K, 1) * V);
   c->dparts = a.arr<float>(8 * B * d);
   c->enc_part = a.arr<float>(B * H * c->nblk_enc * (hd + 2));
+  c->topk_v = a.arr<float>(B * 32 * 8);
+  c->topk_i = a.arr<int>(B * 32 * 8);
   auto meta = [&](TreeMeta& t) {
     t.parent = a.arr<int>(64);
     t.depth = a.arr<int>(64);
@@ -628,7 +632,7 @@ void ctx_dims(chimera_ctx* c) {
   const chimera_config& cf = c->m->cfg;
   c->Mv = std::max(c->B * c->N, 64);
   c->Md = std::max(c->B * (2 * (c->K + 1) + 1), 128);
-  c->G = (c->kv->max_len + 511) / 512 + 1;
+  c->G = (c->kv->max_len + TREE_ATTN_GROUP_POSITIONS - 1) / TREE_ATTN_GROUP_POSITIONS + 1;
   c->tok_stride = c->kv->max_len + 8;
   c->nblk_enc = (2 * c->kv->cap + cf.n_draft_heads + 1 + 255) / 256;
 }

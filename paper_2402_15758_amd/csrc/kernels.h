@@ -69,6 +69,9 @@ void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const 
                     hipStream_t st);
 
 // ---- attention ---------------------------------------------------------------
+// The shared pass of the tree attention writes one partial per group of
+// this many committed positions (4 chunks of 64).
+constexpr int TREE_ATTN_GROUP_POSITIONS = 256;
 struct TreeAttnArgs {
   const void* q;            // [B*N][ldq] rotated queries
   int ldq;
@@ -84,7 +87,7 @@ struct TreeAttnArgs {
   float scale;
   float* part_o;            // [B][H][G][N][hd]
   float* part_ml;           // [B][H][G][N][2]
-  int G;                    // group slots (chunk groups of 8 x 64 positions)
+  int G;                    // group slots (groups of TREE_ATTN_GROUP_POSITIONS positions)
   void* out;                // [B*N][ldo]
   int ldo;
   int B;
@@ -143,7 +146,9 @@ struct StepState {
   int* v_qrow;              // [B*N]
 };
 void launch_argmax(const float* logits, int M, int V, int* amax, hipStream_t st);
-void launch_topk(const float* logits, const StepState& s, int level, hipStream_t st);
+// scratch: [B][32][8] values and ids
+void launch_topk(const float* logits, const StepState& s, int level, float* scratch_v, int* scratch_i,
+                 hipStream_t st);
 void launch_tree_setup(const StepState& s, hipStream_t st);
 void launch_accept(int dtype, const StepState& s, hipStream_t st);
 void launch_compact(int dtype, const StepState& s, void* pool, int n_layers, int64_t layer_stride, hipStream_t st);

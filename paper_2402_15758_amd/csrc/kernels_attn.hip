@@ -7,7 +7,7 @@
 // keys are reduced in 64-position chunks aligned to position 0, in chunk
 // order, with the online softmax:
 //   * chunks 0 .. c_u - 2 (c_u = P_u / 64) hold committed keys only and are
-//     shared by every query of the tree: an MFMA pass over groups of eight
+//     shared by every query of the tree: an MFMA pass over groups of four
 //     chunks writes one partial (m, l, O) per group;
 //   * the last two chunks c_u - 1 and c_u, which contain every tree
 //     position, are reduced per query by a VALU pass that first folds the
@@ -21,7 +21,7 @@
 namespace {
 
 constexpr int CHUNK = 64;   // positions per chunk
-constexpr int GROUP = 8;    // chunks per shared-pass workgroup
+constexpr int GROUP = TREE_ATTN_GROUP_POSITIONS / CHUNK;  // chunks per shared-pass workgroup
 constexpr int TAIL_ROWS = 2 * CHUNK;  // committed rows staged by the tail pass
 constexpr int MAX_NODES = 64;
 
@@ -68,20 +68,36 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   const T* vpool = (const T*)a.vpool;
   const int* ptab = a.page_table + (int64_t)b * a.max_pages;
 
-  for (int c = c_begin; c <= c_end; ++c) {
-    __syncthreads();
-    // stage K rows and V^T of positions 64c .. 64c+63 (all committed)
-    for (int idx = tid; idx < CHUNK * (HD / VEC); idx += 256) {
+  // K rows and V^T of one chunk pass through registers: the global loads of
+  // chunk c+1 are issued before chunk c is reduced.
+  constexpr int PER = CHUNK * (HD / VEC) / 256;
+  int4 kreg[PER], vreg[PER];
+  auto load_chunk = [&](int c) {
+#pragma unroll
+    for (int t = 0; t < PER; ++t) {
+      const int idx = tid + 256 * t;
       const int key = idx % CHUNK, part = idx / CHUNK;
       const int p = c * CHUNK + key;
-      const int64_t base = (int64_t)ptab[p / a.ps] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD + part * VEC;
-      st16(&Ks[key * KP + part * VEC], ld16(kpool + base));
-      const int4 vv = ld16(vpool + base);
-      const T* ve = reinterpret_cast<const T*>(&vv);
+      const int64_t base =
+          (int64_t)ptab[p / a.ps] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD + part * VEC;
+      kreg[t] = ld16(kpool + base);
+      vreg[t] = ld16(vpool + base);
+    }
+  };
+  load_chunk(c_begin);
+  for (int c = c_begin; c <= c_end; ++c) {
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < PER; ++t) {
+      const int idx = tid + 256 * t;
+      const int key = idx % CHUNK, part = idx / CHUNK;
+      st16(&Ks[key * KP + part * VEC], kreg[t]);
+      const T* ve = reinterpret_cast<const T*>(&vreg[t]);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) Vt[(part * VEC + e) * VP + key] = ve[e];
     }
     __syncthreads();
+    if (c < c_end) load_chunk(c + 1);
     if (!wave_on) continue;
 
     f32x4 s[4];
@@ -170,11 +186,12 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tail pass: grid (ceil(N/16), H, B), 4 waves x 4 queries.  Stages the
-// committed rows of the last chunks and all tree slots in LDS.
+// Tail pass: grid (ceil(N/16), H, B), 16 waves; wave w reduces query
+// 16*blockIdx.x + w.  The committed rows of the last chunks and every tree
+// slot are staged in LDS once per workgroup.
 // ---------------------------------------------------------------------------
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
+__global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
   constexpr int VEC = ET<T>::VEC;
   constexpr int KP = HD + VEC;
   constexpr int ROWS = TAIL_ROWS + MAX_NODES;
@@ -194,9 +211,8 @@ __global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
   const T* vpool = (const T*)a.vpool;
   const int* ptab = a.page_table + (int64_t)b * a.max_pages;
 
-  // stage committed rows lo..n-1 into rows 0..nc-1 and tree slots n..n+N-1 into rows 128..
   const int nrows_total = nc + a.N;
-  for (int idx = tid; idx < nrows_total * (HD / VEC); idx += 256) {
+  for (int idx = tid; idx < nrows_total * (HD / VEC); idx += 1024) {
     const int rr = idx / (HD / VEC), part = idx % (HD / VEC);
     const int p = rr < nc ? lo + rr : n + (rr - nc);
     const int dst = rr < nc ? rr : TAIL_ROWS + (rr - nc);
@@ -204,95 +220,92 @@ __global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
     st16(&Kl[dst * KP + part * VEC], ld16(kpool + base));
     st16(&Vl[dst * HD + part * VEC], ld16(vpool + base));
   }
-  __syncthreads();
-
+  const int u = 16 * blockIdx.x + wave;
+  const bool active = u < a.N;
   float* q = qs + wave * HD;
-  // every wave runs the same four iterations so the barriers stay uniform
-  for (int qi = 0; qi < 4; ++qi) {
-    const int u = 16 * blockIdx.x + 4 * wave + qi;
-    const bool active = u < a.N;
-    if (active) {
-      const T* qrow = (const T*)a.q + (int64_t)(b * a.N + u) * a.ldq + h * HD;
-      for (int i = lane; i < HD; i += 64) q[i] = ET<T>::to_f(qrow[i]);
-    }
-    __syncthreads();
-    if (active) {
-      const int Pu = n + a.depth[u];
-      const int cu = Pu / CHUNK;
-      // fold the shared-pass partials in group order
-      float m = -CH_INF, l = 0.f, o[DPL];
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) o[e] = 0.f;
-      const int lim = cu - 2;
-      const int ngrp = lim >= 0 ? lim / GROUP + 1 : 0;
-      for (int gi = 0; gi < ngrp; ++gi) {
-        const int64_t slot = (((int64_t)b * a.H + h) * a.G + gi) * a.N + u;
-        const float mg = a.part_ml[slot * 2], lg = a.part_ml[slot * 2 + 1];
-        if (mg == -CH_INF) continue;
-        const float mn = fmaxf(m, mg);
-        const float a1 = exp_diff(m, mn), a2 = expf(mg - mn);
-        l = l * a1 + lg * a2;
-        const float* po = a.part_o + slot * HD;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + po[DPL * lane + e] * a2;
-        m = mn;
-      }
-      // the last two chunks, keys in logical-position order
-      for (int c = (cu >= 1 ? cu - 1 : 0); c <= cu; ++c) {
-        const int p = c * CHUNK + lane;
-        const bool valid = p <= Pu;
-        int row = 0;
-        float s = -CH_INF;
-        if (valid) {
-          row = p < n ? p - lo : TAIL_ROWS + (int)a.path[u * 64 + (p - n)];
-          const T* kr = &Kl[row * KP];
-          float acc = 0.f;
-#pragma unroll
-          for (int part = 0; part < HD / VEC; ++part) {
-            const int4 kv = ld16(kr + part * VEC);
-            const T* ke = reinterpret_cast<const T*>(&kv);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) acc = fmaf(q[part * VEC + e], ET<T>::to_f(ke[e]), acc);
-          }
-          s = acc * a.scale;
-        }
-        const float mc = wave_max(s);
-        const float mn = fmaxf(m, mc);
-        const float alpha = exp_diff(m, mn);
-        const float pe = valid ? expf(s - mn) : 0.f;
-        l = l * alpha + wave_sum(pe);
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) o[e] = o[e] * alpha;
-        const int cnt = min(CHUNK, Pu - c * CHUNK + 1);
-        for (int i = 0; i < cnt; ++i) {
-          const float pi = __shfl(pe, i);
-          const int ri = __shfl(row, i);
-          const T* vr = &Vl[ri * HD + DPL * lane];
-#pragma unroll
-          for (int e = 0; e < DPL; ++e) o[e] = fmaf(pi, ET<T>::to_f(vr[e]), o[e]);
-        }
-        m = mn;
-      }
-      T* out = (T*)a.out + (int64_t)(b * a.N + u) * a.ldo + h * HD + DPL * lane;
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) out[e] = ET<T>::from_f(o[e] / l);
-    }
-    __syncthreads();
+  if (active) {
+    const T* qrow = (const T*)a.q + (int64_t)(b * a.N + u) * a.ldq + h * HD;
+    for (int i = lane; i < HD; i += 64) q[i] = ET<T>::to_f(qrow[i]);
   }
+  __syncthreads();
+  if (!active) return;
+
+  const int Pu = n + a.depth[u];
+  const int cu = Pu / CHUNK;
+  // fold the shared-pass partials in group order
+  float m = -CH_INF, l = 0.f, o[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) o[e] = 0.f;
+  const int lim = cu - 2;
+  const int ngrp = lim >= 0 ? lim / GROUP + 1 : 0;
+  for (int gi = 0; gi < ngrp; ++gi) {
+    const int64_t slot = (((int64_t)b * a.H + h) * a.G + gi) * a.N + u;
+    const float mg = a.part_ml[slot * 2], lg = a.part_ml[slot * 2 + 1];
+    if (mg == -CH_INF) continue;
+    const float mn = fmaxf(m, mg);
+    const float a1 = exp_diff(m, mn), a2 = expf(mg - mn);
+    l = l * a1 + lg * a2;
+    const float* po = a.part_o + slot * HD;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + po[DPL * lane + e] * a2;
+    m = mn;
+  }
+  // the last two chunks, keys in logical-position order
+  for (int c = (cu >= 1 ? cu - 1 : 0); c <= cu; ++c) {
+    const int p = c * CHUNK + lane;
+    const bool valid = p <= Pu;
+    int row = 0;
+    float s = -CH_INF;
+    if (valid) {
+      row = p < n ? p - lo : TAIL_ROWS + (int)a.path[u * 64 + (p - n)];
+      const T* kr = &Kl[row * KP];
+      float acc = 0.f;
+#pragma unroll
+      for (int part = 0; part < HD / VEC; ++part) {
+        const int4 kv = ld16(kr + part * VEC);
+        const T* ke = reinterpret_cast<const T*>(&kv);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc = fmaf(q[part * VEC + e], ET<T>::to_f(ke[e]), acc);
+      }
+      s = acc * a.scale;
+    }
+    const float mc = wave_max(s);
+    const float mn = fmaxf(m, mc);
+    const float alpha = exp_diff(m, mn);
+    const float pe = valid ? expf(s - mn) : 0.f;
+    l = l * alpha + wave_sum(pe);
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) o[e] = o[e] * alpha;
+    const int cnt = min(CHUNK, Pu - c * CHUNK + 1);
+#pragma unroll
+    for (int i = 0; i < CHUNK; ++i) {
+      if (i < cnt) {
+        const float pi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pe), i));
+        const int ri = __builtin_amdgcn_readlane(row, i);
+        const T* vr = &Vl[ri * HD + DPL * lane];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) o[e] = fmaf(pi, ET<T>::to_f(vr[e]), o[e]);
+      }
+    }
+    m = mn;
+  }
+  T* out = (T*)a.out + (int64_t)(b * a.N + u) * a.ldo + h * HD + DPL * lane;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) out[e] = ET<T>::from_f(o[e] / l);
 }
 
 template <typename T, int HD>
 void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((tree_attn_shared<T, HD>), dim3(a.G, a.H, a.B), dim3(256), 0, st, a);
   constexpr int VEC = ET<T>::VEC;
-  const size_t smem = (size_t)(TAIL_ROWS + MAX_NODES) * ((HD + VEC) + HD) * sizeof(T) + 4 * HD * sizeof(float);
+  const size_t smem = (size_t)(TAIL_ROWS + MAX_NODES) * ((HD + VEC) + HD) * sizeof(T) + 16 * HD * sizeof(float);
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)tree_attn_tail<T, HD>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)smem);
     attr_set = true;
   }
-  hipLaunchKernelGGL((tree_attn_tail<T, HD>), dim3((a.N + 15) / 16, a.H, a.B), dim3(256), smem, st, a);
+  hipLaunchKernelGGL((tree_attn_tail<T, HD>), dim3((a.N + 15) / 16, a.H, a.B), dim3(1024), smem, st, a);
 }
 
 // ---------------------------------------------------------------------------

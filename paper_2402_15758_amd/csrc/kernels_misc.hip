@@ -6,7 +6,6 @@
 
 namespace {
 
-constexpr int MAX_PER_THREAD = 32;  // d <= 8192 with 256 threads
 
 template <typename T>
 __global__ void embed_kernel(const int* __restrict__ tokens, const T* __restrict__ E, float* __restrict__ x, int d,
@@ -27,7 +26,32 @@ __device__ __forceinline__ float block_sum(float v, float* sh) {
   return ((sh[0] + sh[1]) + sh[2]) + sh[3];
 }
 
+// 4 consecutive elements of the storage type as floats / back.
 template <typename T>
+__device__ __forceinline__ float4 ld4f(const T* p);
+template <>
+__device__ __forceinline__ float4 ld4f<float>(const float* p) { return *reinterpret_cast<const float4*>(p); }
+template <>
+__device__ __forceinline__ float4 ld4f<bf16_t>(const bf16_t* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return float4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                __uint_as_float(u.y & 0xffff0000u)};
+}
+template <typename T>
+__device__ __forceinline__ void st4f(T* p, float4 v);
+template <>
+__device__ __forceinline__ void st4f<float>(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+template <>
+__device__ __forceinline__ void st4f<bf16_t>(bf16_t* p, float4 v) {
+  uint2 u;
+  u.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  u.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  *reinterpret_cast<uint2*>(p) = u;
+}
+
+// One workgroup per row; thread t owns the float4 groups t, t+256, ...
+// (NV of them).  Fixed-order sum of squares.
+template <typename T, int NV>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ parts,
                                                       int n_parts, const float* __restrict__ gamma, T* __restrict__ out,
                                                       int ldo, int M, int d, float eps, int write_back,
@@ -35,29 +59,55 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, con
   __shared__ float sh[4];
   const int r = blockIdx.x;
   const bool use_alt = alt != nullptr && r >= alt_begin && r < alt_end;
-  float v[MAX_PER_THREAD];
+  float4 v[NV];
   float ss = 0.f;
-  int c = 0;
-  for (int i = threadIdx.x; i < d; i += 256, ++c) {
-    float val;
-    if (use_alt) {
-      val = ET<T>::to_f(alt[(int64_t)(r - alt_begin) * d + i]);
-    } else {
-      val = x[(int64_t)r * d + i];
-      if (n_parts > 0) {
-        float f = parts[(int64_t)r * d + i];
-        for (int s = 1; s < n_parts; ++s) f = f + parts[((int64_t)s * M + r) * d + i];
-        val = val + f;
-        if (write_back) x[(int64_t)r * d + i] = val;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = 4 * (threadIdx.x + 256 * j);
+    float4 val = float4{0.f, 0.f, 0.f, 0.f};
+    if (i < d) {
+      if (use_alt) {
+        val = ld4f<T>(alt + (int64_t)(r - alt_begin) * d + i);
+      } else {
+        val = *reinterpret_cast<const float4*>(x + (int64_t)r * d + i);
+        if (n_parts > 0) {
+          float4 f = *reinterpret_cast<const float4*>(parts + (int64_t)r * d + i);
+          for (int q = 1; q < n_parts; ++q) {
+            const float4 g = *reinterpret_cast<const float4*>(parts + ((int64_t)q * M + r) * d + i);
+            f.x = f.x + g.x;
+            f.y = f.y + g.y;
+            f.z = f.z + g.z;
+            f.w = f.w + g.w;
+          }
+          val.x = val.x + f.x;
+          val.y = val.y + f.y;
+          val.z = val.z + f.z;
+          val.w = val.w + f.w;
+          if (write_back) *reinterpret_cast<float4*>(x + (int64_t)r * d + i) = val;
+        }
       }
     }
-    v[c] = val;
-    ss = fmaf(val, val, ss);
+    v[j] = val;
+    ss = fmaf(val.x, val.x, ss);
+    ss = fmaf(val.y, val.y, ss);
+    ss = fmaf(val.z, val.z, ss);
+    ss = fmaf(val.w, val.w, ss);
   }
   ss = block_sum(ss, sh);
   const float rinv = 1.0f / sqrtf(ss / (float)d + eps);
-  c = 0;
-  for (int i = threadIdx.x; i < d; i += 256, ++c) out[(int64_t)r * ldo + i] = ET<T>::from_f((v[c] * rinv) * gamma[i]);
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = 4 * (threadIdx.x + 256 * j);
+    if (i < d) {
+      const float4 gm = *reinterpret_cast<const float4*>(gamma + i);
+      float4 o;
+      o.x = (v[j].x * rinv) * gm.x;
+      o.y = (v[j].y * rinv) * gm.y;
+      o.z = (v[j].z * rinv) * gm.z;
+      o.w = (v[j].w * rinv) * gm.w;
+      st4f<T>(out + (int64_t)r * ldo + i, o);
+    }
+  }
 }
 
 // (value, id) order: larger value first, then lower id.
@@ -89,19 +139,23 @@ __device__ __forceinline__ void block_best(float& v, int& i, float* shv, int* sh
     }
 }
 
-__global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ logits, int V, int* __restrict__ amax) {
-  __shared__ float shv[4];
-  __shared__ int shi[4];
+__global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ logits, int V, int* __restrict__ amax) {
+  __shared__ float shv[16];
+  __shared__ int shi[16];
   const int r = blockIdx.x;
   const float* z = logits + (int64_t)r * V;
   float bv = -CH_INF;
   int bi = 0x7fffffff;
-  for (int i = threadIdx.x; i < V; i += 256) {
-    float v = z[i];
-    v = (v != v) ? -CH_INF : v;
-    if (better(v, i, bv, bi)) {
-      bv = v;
-      bi = i;
+  for (int i4 = threadIdx.x; 4 * i4 < V; i4 += 1024) {
+    const float4 q = *reinterpret_cast<const float4*>(z + 4 * i4);
+    const float e[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float v = (e[k] != e[k]) ? -CH_INF : e[k];
+      if (better(v, 4 * i4 + k, bv, bi)) {
+        bv = v;
+        bi = 4 * i4 + k;
+      }
     }
   }
   block_best(bv, bi, shv, shi);
@@ -110,46 +164,138 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ l
 
 // Top-s of draft head `level` for every sequence, with the forced-acceptance
 // rule; the rank-0 entry becomes the chain token at position n + 1 + level.
-__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ logits, StepState s, int level) {
+// Stage 1: TOPK_SPLIT workgroups per sequence keep the best S ids of their
+// slice (excluding the reference id); stage 2 merges them.
+constexpr int TOPK_SPLIT = 32;
+constexpr int SMAX = 8;
+
+__device__ __forceinline__ int forced_ref(const StepState& s, int b, int level, int V, bool* ok) {
+  *ok = false;
+  if (s.f_ref == nullptr) return -1;
+  const int j = s.n[b] + 1 + level;
+  int g = s.f_ref[(int64_t)b * s.f_stride + j];
+  if (g < 0 || g >= V) return -1;
+  *ok = s.f_ok[(int64_t)b * s.f_stride + j] != 0;
+  return g;
+}
+
+__global__ __launch_bounds__(256) void topk_partial_kernel(const float* __restrict__ logits, StepState s, int level,
+                                                           float* __restrict__ pv, int* __restrict__ pi) {
   __shared__ float shv[4];
   __shared__ int shi[4];
-  __shared__ int chosen[8];
-  const int b = blockIdx.x;
+  const int split = blockIdx.x, b = blockIdx.y;
   const int K = s.K, V = s.V;
   const int S = s.s_k[level];
+  bool ok;
+  const int excl = forced_ref(s, b, level, V, &ok);
   const float* z = logits + ((int64_t)b * K + level) * V;
-  const int n = s.n[b];
-  const int j = n + 1 + level;
-  int excl = -1, first = 0;
-  if (s.f_ref != nullptr) {
-    excl = s.f_ref[(int64_t)b * s.f_stride + j];
-    if (excl < 0 || excl >= V) excl = -1;  // no usable reference at this position
-    if (excl >= 0 && s.f_ok[(int64_t)b * s.f_stride + j]) {
-      if (threadIdx.x == 0) chosen[0] = excl;
-      first = 1;
-    }
+  const int lo = (int)((int64_t)V * split / TOPK_SPLIT), hi = (int)((int64_t)V * (split + 1) / TOPK_SPLIT);
+  float lv[SMAX];
+  int li[SMAX];
+#pragma unroll
+  for (int q = 0; q < SMAX; ++q) {
+    lv[q] = -CH_INF;
+    li[q] = 0x7fffffff;
   }
-  for (int r = first; r < S; ++r) {
-    __syncthreads();
-    float bv = -CH_INF;
-    int bi = 0x7fffffff;
-    for (int i = threadIdx.x; i < V; i += 256) {
-      bool skip = i == excl;
-      for (int q = 0; q < r; ++q) skip |= (chosen[q] == i);
-      if (skip) continue;
-      float v = z[i];
-      v = (v != v) ? -CH_INF : v;
-      if (better(v, i, bv, bi)) {
-        bv = v;
-        bi = i;
+  for (int i = lo + threadIdx.x; i < hi; i += 256) {
+    if (i == excl) continue;
+    float v = z[i];
+    v = (v != v) ? -CH_INF : v;
+    if (!better(v, i, lv[SMAX - 1], li[SMAX - 1])) continue;
+    // insert into the sorted local list
+    float cv = v;
+    int ci = i;
+#pragma unroll
+    for (int q = 0; q < SMAX; ++q) {
+      if (better(cv, ci, lv[q], li[q])) {
+        const float tv = lv[q];
+        const int ti = li[q];
+        lv[q] = cv;
+        li[q] = ci;
+        cv = tv;
+        ci = ti;
       }
     }
-    block_best(bv, bi, shv, shi);
-    if (threadIdx.x == 0) chosen[r] = bi < V ? bi : 0;
   }
-  __syncthreads();
-  if (threadIdx.x < S) s.cand[((int64_t)b * K + level) * 8 + threadIdx.x] = chosen[threadIdx.x];
-  if (threadIdx.x == 0) s.tok[(int64_t)b * s.tok_stride + j] = chosen[0];
+  int head = 0;
+  for (int r = 0; r < S; ++r) {
+    float hv = -CH_INF;
+    int hi_ = 0x7fffffff;
+#pragma unroll
+    for (int q = 0; q < SMAX; ++q)
+      if (q == head) {
+        hv = lv[q];
+        hi_ = li[q];
+      }
+    float bv = hv;
+    int bi = hi_;
+    block_best(bv, bi, shv, shi);
+    if (bi == hi_ && hi_ != 0x7fffffff) ++head;
+    if (threadIdx.x == 0) {
+      pv[((int64_t)b * TOPK_SPLIT + split) * SMAX + r] = bv;
+      pi[((int64_t)b * TOPK_SPLIT + split) * SMAX + r] = bi;
+    }
+  }
+}
+
+__global__ __launch_bounds__(64) void topk_merge_kernel(StepState s, int level, const float* __restrict__ pv,
+                                                        const int* __restrict__ pi) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int V = s.V, K = s.K;
+  const int S = s.s_k[level];
+  bool ok;
+  const int g = forced_ref(s, b, level, V, &ok);
+  // lane holds candidates lane, lane+64, ... of the TOPK_SPLIT*S list
+  constexpr int PER = (TOPK_SPLIT * SMAX + 63) / 64;
+  float cv[PER];
+  int ci[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int idx = lane + 64 * q;
+    const int sp = idx / SMAX, r = idx % SMAX;
+    const bool valid = sp < TOPK_SPLIT && r < S;
+    cv[q] = valid ? pv[((int64_t)b * TOPK_SPLIT + sp) * SMAX + r] : -CH_INF;
+    ci[q] = valid ? pi[((int64_t)b * TOPK_SPLIT + sp) * SMAX + r] : 0x7fffffff;
+  }
+  int* out = s.cand + ((int64_t)b * K + level) * 8;
+  int first = 0;
+  if (ok) {
+    if (lane == 0) out[0] = g;
+    first = 1;
+  }
+  int chain = g;
+  for (int r = first; r < S; ++r) {
+    float bv = -CH_INF;
+    int bi = 0x7fffffff;
+    int bq = -1;
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+      if (better(cv[q], ci[q], bv, bi)) {
+        bv = cv[q];
+        bi = ci[q];
+        bq = q;
+      }
+    float wv = bv;
+    int wi = bi;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float ov = __shfl_xor(wv, m);
+      const int oi = __shfl_xor(wi, m);
+      if (better(ov, oi, wv, wi)) {
+        wv = ov;
+        wi = oi;
+      }
+    }
+    if (bq >= 0 && bi == wi) {
+#pragma unroll
+      for (int q = 0; q < PER; ++q)
+        if (q == bq) cv[q] = -CH_INF, ci[q] = 0x7fffffff;
+    }
+    const int id = wi < V ? wi : 0;
+    if (lane == 0) out[r] = id;
+    if (r == 0) chain = id;
+  }
+  if (lane == 0) s.tok[(int64_t)b * s.tok_stride + s.n[b] + 1 + level] = ok ? g : chain;
 }
 
 __global__ void tree_setup_kernel(StepState s) {
@@ -373,23 +519,47 @@ void launch_embed(int dtype, const int* tokens, const void* E, float* x, int M, 
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, st, tokens, (const float*)E, x, d, V);
 }
 
+template <typename T, int NV>
+static void norm_go(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, int M, int d,
+                    float eps, int write_back, const void* alt, int alt_begin, int alt_end, hipStream_t st) {
+  hipLaunchKernelGGL((rmsnorm_kernel<T, NV>), dim3(M), dim3(256), 0, st, x, parts, n_parts, gamma, (T*)out, ldo, M, d,
+                     eps, write_back, (const T*)alt, alt_begin, alt_end);
+}
+
+template <typename T>
+static void norm_t(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, int M, int d,
+                   float eps, int write_back, const void* alt, int alt_begin, int alt_end, hipStream_t st) {
+  switch ((d + 1023) / 1024) {
+    case 1: norm_go<T, 1>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 2: norm_go<T, 2>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 3: norm_go<T, 3>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 4: norm_go<T, 4>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 5: norm_go<T, 5>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 6: norm_go<T, 6>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 7: norm_go<T, 7>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    default: norm_go<T, 8>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+  }
+}
+
 void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, int M,
                     int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end, hipStream_t st) {
   if (M <= 0) return;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(M), dim3(256), 0, st, x, parts, n_parts, gamma, (bf16_t*)out, ldo,
-                       M, d, eps, write_back, (const bf16_t*)alt, alt_begin, alt_end);
+    norm_t<bf16_t>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(M), dim3(256), 0, st, x, parts, n_parts, gamma, (float*)out, ldo, M,
-                       d, eps, write_back, (const float*)alt, alt_begin, alt_end);
+    norm_t<float>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st);
 }
 
 void launch_argmax(const float* logits, int M, int V, int* amax, hipStream_t st) {
-  hipLaunchKernelGGL(argmax_kernel, dim3(M), dim3(256), 0, st, logits, V, amax);
+  hipLaunchKernelGGL(argmax_kernel, dim3(M), dim3(1024), 0, st, logits, V, amax);
 }
 
-void launch_topk(const float* logits, const StepState& s, int level, hipStream_t st) {
-  hipLaunchKernelGGL(topk_kernel, dim3(s.B), dim3(256), 0, st, logits, s, level);
+void launch_topk(const float* logits, const StepState& s, int level, float* scratch_v, int* scratch_i,
+                 hipStream_t st) {
+  hipLaunchKernelGGL(topk_partial_kernel, dim3(TOPK_SPLIT, s.B), dim3(256), 0, st, logits, s, level, scratch_v,
+                     scratch_i);
+  hipLaunchKernelGGL(topk_merge_kernel, dim3(s.B), dim3(64), 0, st, s, level, (const float*)scratch_v,
+                     (const int*)scratch_i);
 }
 
 void launch_tree_setup(const StepState& s, hipStream_t st) {
