@@ -77,3 +77,23 @@ __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x));
 
 // exp(a - b) for the online softmax, with exp(-inf - x) = 0.
 __device__ __forceinline__ float exp_diff(float a, float b) { return (a == -CH_INF) ? 0.0f : expf(a - b); }
+
+// Activations that feed a GEMM are stored in MFMA fragment order: element
+// (row, col) of a matrix with `mtiles` 16-row tiles lives in tile
+// (col / KB, row / 16) at lane ((col % KB) / VEC) * 16 + row % 16, element
+// col % VEC, so that one fragment load is a contiguous 1 KiB.
+template <typename T>
+__device__ __forceinline__ int64_t tiled_index(int mtiles, int row, int col) {
+  constexpr int VEC = ET<T>::VEC, KB = 4 * VEC;
+  const int kb = col / KB, w = col % KB;
+  const int lane = (w / VEC) * 16 + (row & 15);
+  return (((int64_t)kb * mtiles + (row >> 4)) * 64 + lane) * VEC + (w % VEC);
+}
+template <typename T>
+__device__ __forceinline__ void store_tiled(T* base, int mtiles, int row, int col, float v) {
+  base[tiled_index<T>(mtiles, row, col)] = ET<T>::from_f(v);
+}
+template <typename T>
+__device__ __forceinline__ void copy_tiled(T* base, int mtiles, int row, int col, T v) {
+  base[tiled_index<T>(mtiles, row, col)] = v;
+}

@@ -68,6 +68,10 @@ struct Arena {
 
 size_t esize(int dt) { return dt == CHIMERA_BF16 ? 2 : 4; }
 
+// Row capacity of a tiled GEMM-input buffer that may hold up to m rows: a
+// launch with m rows reads 16-row tiles in groups of 1, 2 or 4.
+int mcap(int m) { return m <= 16 ? 16 : (m <= 32 ? 32 : (m + 63) / 64 * 64); }
+
 struct BlockW {
   float* attn_norm = nullptr;
   void* wqkv = nullptr;
@@ -84,8 +88,8 @@ void validate_config(const chimera_config* c) {
   REQUIRE(c->head_dim == 64 || c->head_dim == 128, CHIMERA_EINVAL, "head_dim must be 64 or 128");
   REQUIRE(c->n_heads * c->head_dim == c->d_model, CHIMERA_EINVAL, "n_heads * head_dim != d_model");
   REQUIRE(c->d_model % 256 == 0 && c->d_model <= 8192, CHIMERA_EINVAL, "d_model must be a multiple of 256, <= 8192");
-  REQUIRE(c->d_ffn % 32 == 0 && c->d_ffn % 64 == 0, CHIMERA_EINVAL, "d_ffn must be a multiple of 64");
-  REQUIRE(c->vocab % 32 == 0 && c->vocab >= 32, CHIMERA_EINVAL, "vocab must be a multiple of 32");
+  REQUIRE(c->d_ffn % 64 == 0, CHIMERA_EINVAL, "d_ffn must be a multiple of 64");
+  REQUIRE(c->vocab % 64 == 0 && c->vocab >= 64, CHIMERA_EINVAL, "vocab must be a multiple of 64");
   REQUIRE(c->n_draft_heads >= 0 && c->n_draft_heads <= 8, CHIMERA_EINVAL, "n_draft_heads in [0, 8]");
   REQUIRE(c->max_positions >= 16, CHIMERA_EINVAL, "max_positions");
   REQUIRE(c->rms_eps > 0.f && c->rope_base > 1.f, CHIMERA_EINVAL, "eps/base");
@@ -170,7 +174,9 @@ struct chimera_ctx {
   float* scratch = nullptr;
   float* logits = nullptr;
   int* amax = nullptr;
-  void* hl = nullptr;
+  void* hl = nullptr;      // tiled (LM head input)
+  void* hl_rm = nullptr;   // row-major copy (decode state)
+  int mt_v = 0, mt_d = 0, mt_b = 0;  // 16-row tiles of the verify, draft and per-sequence buffers
   float* part_o = nullptr;
   float* part_ml = nullptr;
   int* v_pos = nullptr;
@@ -261,11 +267,11 @@ struct Gemm {
   hipStream_t st;
   bool timed;  // record events around the launch (verify GEMMs while profiling)
 
-  void run(const void* X, int ldx, int M, const void* W, int N, int K, GemmEpi e, int nb_off = 0,
+  void run(const void* X, int x_mtiles, int M, const void* W, int N, int K, GemmEpi e, int nb_off = 0,
            int nb_count = 0) const {
     GemmShape s;
     s.X = X;
-    s.ldx = ldx;
+    s.x_mtiles = x_mtiles;
     s.M = M;
     s.W = W;
     s.N = N;
@@ -274,7 +280,9 @@ struct Gemm {
     s.nb_count = nb_count;
     const int cols = nb_count ? nb_count * 16 : N;
     s.splits = gemm_pick_splits(cols, K, c->m->dt);
-    if (e.kind == EPI_PARTIAL) REQUIRE(s.splits <= 8, CHIMERA_EINVAL, "splits");
+    const int tiles_read = M <= 16 ? 1 : (M <= 32 ? 2 : 4 * ((M + 63) / 64));
+    REQUIRE(tiles_read <= x_mtiles, CHIMERA_EINVAL, "GEMM rows exceed the input buffer");
+    if (e.kind != EPI_PARTIAL) e.part = c->scratch;
     Event2* ev = nullptr;
     if (timed && c->prof && c->ev_used < c->ev_pool.size()) {
       ev = &c->ev_pool[c->ev_used];
@@ -283,7 +291,7 @@ struct Gemm {
       c->ev_used++;
       HIPCK(hipEventRecord(ev->a, st));
     }
-    launch_gemm(c->m->dt, s, e, c->scratch, st);
+    launch_gemm(c->m->dt, s, e, st);
     if (ev) HIPCK(hipEventRecord(ev->b, st));
   }
   int splits(int N, int K) const { return gemm_pick_splits(N, K, c->m->dt); }
@@ -311,8 +319,8 @@ void verify_layers(chimera_ctx* c, const VerifyRows& r, hipStream_t st, bool tim
   int nparts = 0;
   for (int l = 0; l < cf.n_layers; ++l) {
     const BlockW& w = m->layers[l];
-    launch_rmsnorm(dt, c->x, nparts ? c->parts : nullptr, nparts, w.attn_norm, c->xn, d, r.M, d, cf.rms_eps, 1,
-                   nullptr, 0, 0, st);
+    launch_rmsnorm(dt, c->x, nparts ? c->parts : nullptr, nparts, w.attn_norm, c->xn, c->mt_v, nullptr, r.M, d,
+                   cf.rms_eps, 1, nullptr, 0, 0, st);
     char* kbase = (char*)kv->pool + (size_t)l * kv->layer_stride * m->es;
     char* vbase = kbase + (size_t)H * kv->ps * hd * m->es;
     GemmEpi e;
@@ -329,7 +337,7 @@ void verify_layers(chimera_ctx* c, const VerifyRows& r, hipStream_t st, bool tim
     e.rsin = m->rsin;
     e.H = H;
     e.hd = hd;
-    g.run(c->xn, d, r.M, w.wqkv, 3 * hdim, d, e);
+    g.run(c->xn, c->mt_v, r.M, w.wqkv, 3 * hdim, d, e);
 
     TreeAttnArgs a{};
     a.q = c->q;
@@ -352,28 +360,30 @@ void verify_layers(chimera_ctx* c, const VerifyRows& r, hipStream_t st, bool tim
     a.part_ml = c->part_ml;
     a.G = c->G;
     a.out = c->attn;
-    a.ldo = hdim;
+    a.o_mtiles = c->mt_v;
     a.B = r.B;
     launch_tree_attn(dt, a, st);
 
     GemmEpi eo;
     eo.kind = EPI_PARTIAL;
     eo.part = c->parts;
-    g.run(c->attn, hdim, r.M, w.wo, d, hdim, eo);
+    g.run(c->attn, c->mt_v, r.M, w.wo, d, hdim, eo);
     nparts = g.splits(d, hdim);
-    launch_rmsnorm(dt, c->x, c->parts, nparts, w.ffn_norm, c->xn, d, r.M, d, cf.rms_eps, 1, nullptr, 0, 0, st);
+    launch_rmsnorm(dt, c->x, c->parts, nparts, w.ffn_norm, c->xn, c->mt_v, nullptr, r.M, d, cf.rms_eps, 1, nullptr, 0,
+                   0, st);
     GemmEpi egu;
     egu.kind = EPI_SWIGLU;
     egu.out_t = c->hbuf;
-    egu.ldo = F;
-    g.run(c->xn, d, r.M, w.wgu, 2 * F, d, egu);
+    egu.o_mtiles = c->mt_v;
+    g.run(c->xn, c->mt_v, r.M, w.wgu, 2 * F, d, egu);
     GemmEpi ed;
     ed.kind = EPI_PARTIAL;
     ed.part = c->parts;
-    g.run(c->hbuf, F, r.M, w.wdown, d, F, ed);
+    g.run(c->hbuf, c->mt_v, r.M, w.wdown, d, F, ed);
     nparts = g.splits(d, F);
   }
-  launch_rmsnorm(dt, c->x, c->parts, nparts, m->final_norm, c->hl, d, r.M, d, cf.rms_eps, 1, nullptr, 0, 0, st);
+  launch_rmsnorm(dt, c->x, c->parts, nparts, m->final_norm, c->hl, c->mt_v, c->hl_rm, r.M, d, cf.rms_eps, 1, nullptr,
+                 0, 0, st);
 }
 
 StepState make_state(chimera_ctx* c) {
@@ -414,7 +424,7 @@ StepState make_state(chimera_ctx* c) {
   s.pro_base = c->pro_base;
   s.pro_count = c->pro_count;
   s.pro_h = c->pro_h;
-  s.hl = c->hl;
+  s.hl = c->hl_rm;
   s.amax = c->amax;
   s.v_pos = c->v_pos;
   s.v_kvoff = c->v_kvoff;
@@ -432,18 +442,18 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
   const Gemm g{c, st, false};
   for (int k = 0; k < K; ++k) {
     const int Mk = k == 0 ? B * (2 * (K + 1) + 1) : B;
-    launch_draft_rows(dt, s, m->embed, k, c->tri_in, c->d_pos, c->d_kvoff, c->d_qrow, st);
+    launch_draft_rows(dt, s, m->embed, k, c->tri_in, c->mt_d, c->d_pos, c->d_kvoff, c->d_qrow, st);
     GemmEpi e1;
     e1.kind = EPI_SILU;
     e1.out_t = c->tri_a;
-    e1.ldo = d;
-    g.run(c->tri_in, 3 * d, Mk, m->tri_w1, d, 3 * d, e1);
+    e1.o_mtiles = c->mt_d;
+    g.run(c->tri_in, c->mt_d, Mk, m->tri_w1, d, 3 * d, e1);
     GemmEpi e2;
     e2.kind = EPI_F32;
     e2.out_f = c->htri;
     e2.ldo = d;
-    g.run(c->tri_a, d, Mk, m->tri_w2, d, d, e2);
-    launch_rmsnorm(dt, c->htri, nullptr, 0, m->enc.attn_norm, c->un, d, Mk, d, cf.rms_eps, 0,
+    g.run(c->tri_a, c->mt_d, Mk, m->tri_w2, d, d, e2);
+    launch_rmsnorm(dt, c->htri, nullptr, 0, m->enc.attn_norm, c->un, c->mt_d, nullptr, Mk, d, cf.rms_eps, 0,
                    k == 0 ? c->pro_h : nullptr, B, B + B * (K + 1), st);
     GemmEpi eq;
     eq.kind = EPI_QKV;
@@ -459,7 +469,7 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
     eq.rsin = m->rsin;
     eq.H = H;
     eq.hd = hd;
-    g.run(c->un, d, Mk, m->enc.wqkv, 3 * hdim, d, eq);
+    g.run(c->un, c->mt_d, Mk, m->enc.wqkv, 3 * hdim, d, eq);
 
     EncAttnArgs ea{};
     ea.q = c->qc;
@@ -475,36 +485,36 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
     ea.part = c->enc_part;
     ea.nblk = c->nblk_enc;
     ea.out = c->attn_c;
-    ea.ldo = hdim;
+    ea.o_mtiles = c->mt_b;
     ea.B = B;
     launch_enc_attn(dt, ea, st);
 
     GemmEpi eo;
     eo.kind = EPI_PARTIAL;
     eo.part = c->dparts;
-    g.run(c->attn_c, hdim, B, m->enc.wo, d, hdim, eo);
-    launch_rmsnorm(dt, c->htri, c->dparts, g.splits(d, hdim), m->enc.ffn_norm, c->yn, d, B, d, cf.rms_eps, 1,
-                   nullptr, 0, 0, st);
+    g.run(c->attn_c, c->mt_b, B, m->enc.wo, d, hdim, eo);
+    launch_rmsnorm(dt, c->htri, c->dparts, g.splits(d, hdim), m->enc.ffn_norm, c->yn, c->mt_b, nullptr, B, d,
+                   cf.rms_eps, 1, nullptr, 0, 0, st);
     GemmEpi egu;
     egu.kind = EPI_SWIGLU;
     egu.out_t = c->hc;
-    egu.ldo = F;
-    g.run(c->yn, d, B, m->enc.wgu, 2 * F, d, egu);
+    egu.o_mtiles = c->mt_b;
+    g.run(c->yn, c->mt_b, B, m->enc.wgu, 2 * F, d, egu);
     GemmEpi ed;
     ed.kind = EPI_PARTIAL;
     ed.part = c->dparts;
-    g.run(c->hc, F, B, m->enc.wdown, d, F, ed);
-    launch_draft_finish(dt, s, c->htri, c->dparts, g.splits(d, F), c->zin, st);
+    g.run(c->hc, c->mt_b, B, m->enc.wdown, d, F, ed);
+    launch_draft_finish(dt, s, c->htri, c->dparts, g.splits(d, F), c->zin, c->mt_b, st);
     GemmEpi ea1;
     ea1.kind = EPI_SILU;
     ea1.out_t = c->ak;
-    ea1.ldo = d;
-    g.run(c->zin, 2 * d, B, m->head_a[k], d, 2 * d, ea1);
+    ea1.o_mtiles = c->mt_b;
+    g.run(c->zin, c->mt_b, B, m->head_a[k], d, 2 * d, ea1);
     GemmEpi et;
     et.kind = EPI_F32;
     et.out_f = c->dlogits + (size_t)k * V;
     et.ldo = K * V;
-    g.run(c->ak, d, B, m->head_theta[k], V, d, et);
+    g.run(c->ak, c->mt_b, B, m->head_theta[k], V, d, et);
     launch_topk(c->dlogits, s, k, c->topk_v, c->topk_i, st);
   }
 }
@@ -529,6 +539,10 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   const chimera_config& cf = m->cfg;
   const size_t es = m->es, d = cf.d_model, F = cf.d_ffn, V = cf.vocab, H = cf.n_heads, hd = cf.head_dim;
   const size_t B = c->B, K = c->K, Mv = c->Mv, Md = c->Md, N = c->N;
+  const size_t Bp = (size_t)mcap(c->B);
+  c->mt_v = (int)(Mv / 16);
+  c->mt_d = (int)(Md / 16);
+  c->mt_b = (int)(Bp / 16);
   c->n = a.arr<int>(B);
   c->tok = a.arr<int>(B * c->tok_stride);
   c->h_last = a.take(B * d * es);
@@ -559,7 +573,7 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
     if (s > 1) scr = std::max(scr, (size_t)s * M * (size_t)n_full);
   };
   const int hdim = (int)(H * hd);
-  for (size_t M : {Mv, Md, B, (size_t)128}) {
+  for (size_t M : {Mv, Md, Bp, (size_t)128}) {
     need(M, 3 * hdim, 3 * hdim, (int)d);
     need(M, 2 * hdim, 3 * hdim, (int)d);
     need(M, 2 * (int)F, 2 * (int)F, (int)d);
@@ -572,6 +586,7 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   c->logits = a.arr<float>(Mv * V);
   c->amax = a.arr<int>(Mv);
   c->hl = a.take(Mv * d * es);
+  c->hl_rm = a.take(Mv * d * es);
   const size_t qrows = std::max(B * N, (size_t)64);
   c->part_o = a.arr<float>(qrows * H * c->G * hd);
   c->part_ml = a.arr<float>(qrows * H * c->G * 2);
@@ -586,11 +601,11 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   c->d_kvoff = a.arr<int64_t>(Md);
   c->d_qrow = a.arr<int>(Md);
   c->qc = a.take(Md * d * es);
-  c->attn_c = a.take(B * d * es);
-  c->yn = a.take(B * d * es);
-  c->hc = a.take(B * F * es);
-  c->zin = a.take(B * 2 * d * es);
-  c->ak = a.take(B * d * es);
+  c->attn_c = a.take(Bp * d * es);
+  c->yn = a.take(Bp * d * es);
+  c->hc = a.take(Bp * F * es);
+  c->zin = a.take(Bp * 2 * d * es);
+  c->ak = a.take(Bp * d * es);
   c->dlogits = a.arr<float>(B * std::max<size_t>(K, 1) * V);
   c->dparts = a.arr<float>(8 * B * d);
   c->enc_part = a.arr<float>(B * H * c->nblk_enc * (hd + 2));
@@ -630,8 +645,8 @@ void upload_meta(TreeMeta& t, const std::vector<int>& parent, const std::vector<
 
 void ctx_dims(chimera_ctx* c) {
   const chimera_config& cf = c->m->cfg;
-  c->Mv = std::max(c->B * c->N, 64);
-  c->Md = std::max(c->B * (2 * (c->K + 1) + 1), 128);
+  c->Mv = mcap(std::max(c->B * c->N, 64));
+  c->Md = mcap(std::max(c->B * (2 * (c->K + 1) + 1), 128));
   c->G = (c->kv->max_len + TREE_ATTN_GROUP_POSITIONS - 1) / TREE_ATTN_GROUP_POSITIONS + 1;
   c->tok_stride = c->kv->max_len + 8;
   c->nblk_enc = (2 * c->kv->cap + cf.n_draft_heads + 1 + 255) / 256;
@@ -1002,8 +1017,8 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
       off += n;
       for (int p0 = 0; p0 < n; p0 += 64) {
         const int M = std::min(64, n - p0);
-        launch_prefill_rows(dt, s, m->embed, b, p0, M, ctx->pf_tokens, ctx->tri_in, ctx->d_pos, ctx->d_kvoff,
-                            ctx->d_qrow, ctx->pf_n, st);
+        launch_prefill_rows(dt, s, m->embed, b, p0, M, ctx->pf_tokens, ctx->tri_in, ctx->mt_d, ctx->d_pos,
+                            ctx->d_kvoff, ctx->d_qrow, ctx->pf_n, st);
         VerifyRows r{ctx->pf_tokens, M, ctx->pf_n, kv->page_table + (size_t)b * kv->max_pages,
                      ctx->chain.depth, ctx->chain.path, M, M - 1, 1};
         verify_layers(ctx, r, st, false);
@@ -1011,15 +1026,15 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
         GemmEpi e1;
         e1.kind = EPI_SILU;
         e1.out_t = ctx->tri_a;
-        e1.ldo = d;
-        g.run(ctx->tri_in, 3 * d, M, m->tri_w1, d, 3 * d, e1);
+        e1.o_mtiles = ctx->mt_d;
+        g.run(ctx->tri_in, ctx->mt_d, M, m->tri_w1, d, 3 * d, e1);
         GemmEpi e2;
         e2.kind = EPI_F32;
         e2.out_f = ctx->htri + (size_t)M * d;
         e2.ldo = d;
-        g.run(ctx->tri_a, d, M, m->tri_w2, d, d, e2);
-        launch_rmsnorm(dt, ctx->htri, nullptr, 0, m->enc.attn_norm, ctx->un, d, 2 * M, d, cf.rms_eps, 0, ctx->hl, 0, M,
-                       st);
+        g.run(ctx->tri_a, ctx->mt_d, M, m->tri_w2, d, d, e2);
+        launch_rmsnorm(dt, ctx->htri, nullptr, 0, m->enc.attn_norm, ctx->un, ctx->mt_d, nullptr, 2 * M, d, cf.rms_eps,
+                       0, ctx->hl_rm, 0, M, st);
         GemmEpi ekv;
         ekv.kind = EPI_QKV;
         ekv.pos = ctx->d_pos;
@@ -1034,15 +1049,15 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
         ekv.rsin = m->rsin;
         ekv.H = H;
         ekv.hd = hd;
-        g.run(ctx->un, d, 2 * M, m->enc.wqkv, 3 * hdim, d, ekv, hdim / 16, 2 * hdim / 16);
+        g.run(ctx->un, ctx->mt_d, 2 * M, m->enc.wqkv, 3 * hdim, d, ekv, hdim / 16, 2 * hdim / 16);
         if (p0 + M == n) {
           GemmEpi el;
           el.kind = EPI_F32;
           el.out_f = ctx->logits;
           el.ldo = V;
-          const char* last = (const char*)ctx->hl + (size_t)(M - 1) * d * m->es;
-          g.run(last, d, 1, m->lm_head, V, d, el);
-          launch_argmax(ctx->logits, 1, V, ctx->amax, st);
+          g.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
+          launch_argmax(ctx->logits + (size_t)(M - 1) * V, 1, V, ctx->amax, st);
+          const char* last = (const char*)ctx->hl_rm + (size_t)(M - 1) * d * m->es;
           launch_prefill_finish(dt, s, b, n, ctx->amax, last, st);
         }
       }
@@ -1101,7 +1116,7 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
     el.kind = EPI_F32;
     el.out_f = ctx->logits;
     el.ldo = V;
-    g.run(ctx->hl, d, M, m->lm_head, V, d, el);
+    g.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
     launch_argmax(ctx->logits, M, V, ctx->amax, st);
     if (ctx->prof) HIPCK(hipEventRecord(ctx->e_verify, st));
     launch_accept(dt, s, st);
@@ -1245,26 +1260,30 @@ chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, i
     REQUIRE(dtype == CHIMERA_F32 || dtype == CHIMERA_BF16, CHIMERA_EINVAL, "dtype");
     REQUIRE(x && w && y, CHIMERA_EINVAL, "null argument");
     const int KB = dtype == CHIMERA_BF16 ? 32 : 16;
-    REQUIRE(M >= 1 && M <= 256 && N % 32 == 0 && N > 0 && K % KB == 0 && K > 0, CHIMERA_EINVAL,
-            "M in [1, 256], N % 32 == 0, K % KB == 0");
+    REQUIRE(M >= 1 && M <= 256 && N % 64 == 0 && N > 0 && K % KB == 0 && K > 0, CHIMERA_EINVAL,
+            "M in [1, 256], N % 64 == 0, K % KB == 0");
     const size_t es = esize(dtype);
-    void *dx = nullptr, *dw = nullptr, *dp = nullptr, *dy = nullptr, *ds = nullptr;
+    void *dx = nullptr, *dxr = nullptr, *dw = nullptr, *dp = nullptr, *dy = nullptr, *ds = nullptr;
     auto cleanup = [&] {
-      for (void* p : {dx, dw, dp, dy, ds})
+      for (void* p : {dx, dxr, dw, dp, dy, ds})
         if (p) (void)hipFree(p);
     };
     try {
-      HIPCK(hipMalloc(&dx, (size_t)M * K * es));
+      const int mc = mcap(M);
+      HIPCK(hipMalloc(&dx, (size_t)mc * K * es));
+      HIPCK(hipMemset(dx, 0, (size_t)mc * K * es));
       HIPCK(hipMalloc(&dw, (size_t)K * N * es));
       HIPCK(hipMalloc(&dp, (size_t)K * N * es));
       HIPCK(hipMalloc(&dy, (size_t)M * N * 4));
-      HIPCK(hipMalloc(&ds, (size_t)8 * M * N * 4));
-      HIPCK(hipMemcpy(dx, x, (size_t)M * K * es, hipMemcpyHostToDevice));
+      HIPCK(hipMalloc(&ds, (size_t)8 * M * N * 4 + 65536 * 4));
+      HIPCK(hipMalloc(&dxr, (size_t)M * K * es));
+      HIPCK(hipMemcpy(dxr, x, (size_t)M * K * es, hipMemcpyHostToDevice));
+      launch_tile_rows(dtype, dxr, M, K, dx, mc / 16, nullptr);
       HIPCK(hipMemcpy(dw, w, (size_t)K * N * es, hipMemcpyHostToDevice));
       launch_repack(dtype, PACK_NATURAL, dw, nullptr, nullptr, K, N, dp, 1, 64, nullptr);
       GemmShape s;
       s.X = dx;
-      s.ldx = K;
+      s.x_mtiles = mc / 16;
       s.M = M;
       s.W = dp;
       s.N = N;
@@ -1274,7 +1293,8 @@ chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, i
       e.kind = EPI_F32;
       e.out_f = (float*)dy;
       e.ldo = N;
-      launch_gemm(dtype, s, e, (float*)ds, nullptr);
+      e.part = (float*)ds;
+      launch_gemm(dtype, s, e, nullptr);
       HIPCK(hipGetLastError());
       HIPCK(hipDeviceSynchronize());
       HIPCK(hipMemcpy(y, dy, (size_t)M * N * 4, hipMemcpyDeviceToHost));

@@ -22,10 +22,12 @@ enum { EPI_F32 = 0, EPI_T = 1, EPI_SILU = 2, EPI_SWIGLU = 3, EPI_QKV = 4, EPI_PA
 
 struct GemmEpi {
   int kind = EPI_F32;
-  float* out_f = nullptr;  // EPI_F32: [M][ldo]
-  void* out_t = nullptr;   // EPI_T / EPI_SILU / EPI_SWIGLU: [M][ldo] of the storage type
+  float* out_f = nullptr;  // EPI_F32: row-major [M][ldo]
   int ldo = 0;
-  float* part = nullptr;   // EPI_PARTIAL: [splits][M][N] (packed column order)
+  void* out_t = nullptr;   // EPI_T / EPI_SILU / EPI_SWIGLU: tiled storage-type output
+  int o_mtiles = 0;        //   with this many 16-row tiles
+  float* part = nullptr;   // EPI_PARTIAL: [splits][M][N] (packed column order); other
+                           // epilogues with split-K: scratch of the same shape
   // EPI_QKV: per-row rotary position, KV element offset (-1: skip) and
   // Q output row (-1: skip); K/V go to kbase/vbase + kvoff + h*head_stride.
   const int* pos = nullptr;
@@ -34,7 +36,7 @@ struct GemmEpi {
   void* kbase = nullptr;
   void* vbase = nullptr;
   int64_t head_stride = 0;
-  void* qout = nullptr;
+  void* qout = nullptr;    // row-major [rows][ldq]
   int ldq = 0;
   const float* rcos = nullptr;  // [max_pos][hd/2]
   const float* rsin = nullptr;
@@ -42,31 +44,34 @@ struct GemmEpi {
 };
 
 struct GemmShape {
-  const void* X = nullptr;
-  int ldx = 0;
+  const void* X = nullptr;  // tiled activations
+  int x_mtiles = 0;         // 16-row tiles of X's buffer
   int M = 0;
   const void* W = nullptr;  // packed
   int N = 0;                // packed columns of the whole matrix
   int K = 0;
-  int nb_off = 0;           // first 16-column block to compute (even)
-  int nb_count = 0;         // number of 16-column blocks to compute (even); 0 = all
+  int nb_off = 0;           // first 16-column block to compute (multiple of 4)
+  int nb_count = 0;         // number of 16-column blocks to compute (multiple of 4); 0 = all
   int splits = 1;           // split of the reduction across workgroups
 };
 
 // Splits chosen from (N, K) only, never from M.
 int gemm_pick_splits(int n_cols, int K, int dtype);
-void launch_gemm(int dtype, const GemmShape& s, const GemmEpi& e, float* scratch, hipStream_t st);
+void launch_gemm(int dtype, const GemmShape& s, const GemmEpi& e, hipStream_t st);
 void launch_repack(int dtype, int kind, const void* src0, const void* src1, const void* src2, int K, int n_src,
                    void* dst, int H, int hd, hipStream_t st);
+// Row-major [M][K] -> tiled (test hook and one-off conversions).
+void launch_tile_rows(int dtype, const void* src, int M, int K, void* dst, int mtiles, hipStream_t st);
 
 // ---- elementwise / norms ------------------------------------------------------
 void launch_embed(int dtype, const int* tokens, const void* E, float* x, int M, int d, int V, hipStream_t st);
-// x[r] += sum_s parts[s][r] (if parts), optionally written back; out[r] =
-// T(rmsnorm(x[r]) * gamma).  Rows r in [alt_begin, alt_end) read their input
-// from alt[(r - alt_begin)] (storage type) instead of x.
-void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo,
-                    int M, int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end,
-                    hipStream_t st);
+// x[r] += sum_s parts[s][r] (if parts), optionally written back; out (tiled,
+// o_mtiles tiles) row r = T(rmsnorm(x[r]) * gamma), and the same values
+// row-major into out_rm if given.  Rows r in [alt_begin, alt_end) read their
+// input from row-major alt[(r - alt_begin)] (storage type) instead of x.
+void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const float* gamma, void* out, int o_mtiles,
+                    void* out_rm, int M, int d, float eps, int write_back, const void* alt, int alt_begin,
+                    int alt_end, hipStream_t st);
 
 // ---- attention ---------------------------------------------------------------
 // The shared pass of the tree attention writes one partial per group of
@@ -88,8 +93,8 @@ struct TreeAttnArgs {
   float* part_o;            // [B][H][G][N][hd]
   float* part_ml;           // [B][H][G][N][2]
   int G;                    // group slots (groups of TREE_ATTN_GROUP_POSITIONS positions)
-  void* out;                // [B*N][ldo]
-  int ldo;
+  void* out;                // tiled [B*N][H*hd] with o_mtiles tiles
+  int o_mtiles;
   int B;
 };
 void launch_tree_attn(int dtype, const TreeAttnArgs& a, hipStream_t st);
@@ -106,8 +111,8 @@ struct EncAttnArgs {
   float scale;
   float* part;              // [B][H][nblk][hd + 2]
   int nblk;
-  void* out;                // [B][ldo]
-  int ldo;
+  void* out;                // tiled [B][H*hd] with o_mtiles tiles
+  int o_mtiles;
   int B;
 };
 void launch_enc_attn(int dtype, const EncAttnArgs& a, hipStream_t st);
@@ -138,7 +143,7 @@ struct StepState {
   int* pro_base;            // [B]
   int* pro_count;           // [B]
   void* pro_h;              // [B][K+1][d]
-  const void* hl;           // [B*N][d] post-final-norm verify states
+  const void* hl;           // [B*N][d] post-final-norm verify states (row-major)
   const int* amax;          // [B*N]
   // verify row descriptors
   int* v_pos;               // [B*N]
@@ -159,17 +164,18 @@ void launch_advance(int dtype, const StepState& s, hipStream_t st);
 // previous step's committed target-state entries and rows
 // [B + B(K+1), B + 2B(K+1)) their trigram entries.  Writes the trigram
 // inputs [rows][3d], rotary positions, encoder-memory offsets and Q rows.
-void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int* pos,
-                       int64_t* kvoff, int* qrow, hipStream_t st);
-// zin[b] = [h_last[b]; T(x[b] + sum_s parts[s][b])]
+void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int tri_mtiles,
+                       int* pos, int64_t* kvoff, int* qrow, hipStream_t st);
+// zin[b] (tiled) = [h_last[b]; T(x[b] + sum_s parts[s][b])]
 void launch_draft_finish(int dtype, const StepState& s, const float* x, const float* parts, int n_parts, void* zin,
-                         hipStream_t st);
+                         int z_mtiles, hipStream_t st);
 // Prefill chunk rows: positions p0 .. p0+M-1 of sequence b; writes verify
 // descriptors (pos, kvoff through the page table, qrow), the token list,
 // trigram inputs for the same positions and the encoder descriptors of the
 // target-state rows [0, M) and trigram rows [M, 2M).
 void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, int p0, int M, int* tokens_out,
-                         void* tri_in, int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n, hipStream_t st);
+                         void* tri_in, int tri_mtiles, int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n,
+                         hipStream_t st);
 // Prefill end: pending token, h_last, committed length and tokens.
 void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,
                            hipStream_t st);

@@ -289,9 +289,8 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
     }
     m = mn;
   }
-  T* out = (T*)a.out + (int64_t)(b * a.N + u) * a.ldo + h * HD + DPL * lane;
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) out[e] = ET<T>::from_f(o[e] / l);
+  for (int e = 0; e < DPL; ++e) store_tiled<T>((T*)a.out, a.o_mtiles, b * a.N + u, h * HD + DPL * lane + e, o[e] / l);
 }
 
 template <typename T, int HD>
@@ -412,9 +411,8 @@ __global__ void enc_attn_combine(const EncAttnArgs a) {
     for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + src[DPL * lane + e] * a2;
     m = mn;
   }
-  T* out = (T*)a.out + (int64_t)b * a.ldo + h * HD + DPL * lane;
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) out[e] = ET<T>::from_f(o[e] / l);
+  for (int e = 0; e < DPL; ++e) store_tiled<T>((T*)a.out, a.o_mtiles, b, h * HD + DPL * lane + e, o[e] / l);
 }
 
 template <typename T, int HD>

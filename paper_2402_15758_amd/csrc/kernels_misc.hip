@@ -54,8 +54,9 @@ __device__ __forceinline__ void st4f<bf16_t>(bf16_t* p, float4 v) {
 template <typename T, int NV>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ parts,
                                                       int n_parts, const float* __restrict__ gamma, T* __restrict__ out,
-                                                      int ldo, int M, int d, float eps, int write_back,
-                                                      const T* __restrict__ alt, int alt_begin, int alt_end) {
+                                                      int o_mtiles, T* __restrict__ out_rm, int M, int d, float eps,
+                                                      int write_back, const T* __restrict__ alt, int alt_begin,
+                                                      int alt_end) {
   __shared__ float sh[4];
   const int r = blockIdx.x;
   const bool use_alt = alt != nullptr && r >= alt_begin && r < alt_end;
@@ -105,7 +106,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, con
       o.y = (v[j].y * rinv) * gm.y;
       o.z = (v[j].z * rinv) * gm.z;
       o.w = (v[j].w * rinv) * gm.w;
-      st4f<T>(out + (int64_t)r * ldo + i, o);
+      // 4 consecutive columns stay inside one lane's fragment chunk
+      st4f<T>(out + tiled_index<T>(o_mtiles, r, i), o);
+      if (out_rm != nullptr) st4f<T>(out_rm + (int64_t)r * d + i, o);
     }
   }
 }
@@ -405,15 +408,18 @@ __global__ __launch_bounds__(256) void advance_kernel(StepState s) {
   }
 }
 
+// Trigram input t = [e(pos-2); e(pos-1); e(pos)] of one row, zero vectors
+// before the sequence start, written tiled.
 template <typename T>
-__device__ __forceinline__ void trigram_row(const StepState& s, const T* E, int b, int pos, T* dst) {
+__device__ __forceinline__ void trigram_row(const StepState& s, const T* E, int b, int pos, T* dst, int mtiles,
+                                            int row) {
   const int d = s.d;
   for (int i = threadIdx.x; i < 3 * d; i += blockDim.x) {
     const int part = i / d, col = i % d;
     const int p = pos - 2 + part;
     T v = ET<T>::from_f(0.f);
     if (p >= 0) v = E[(int64_t)s.tok[(int64_t)b * s.tok_stride + p] * d + col];
-    dst[i] = v;
+    copy_tiled<T>(dst, mtiles, row, i, v);
   }
 }
 
@@ -422,8 +428,8 @@ __device__ __forceinline__ int64_t enc_off(const StepState& s, int b, int stream
 }
 
 template <typename T>
-__global__ void draft_rows_kernel(StepState s, const T* E, int level, T* tri_in, int* pos, int64_t* kvoff,
-                                  int* qrow) {
+__global__ void draft_rows_kernel(StepState s, const T* E, int level, T* tri_in, int tri_mtiles, int* pos,
+                                  int64_t* kvoff, int* qrow) {
   const int r = blockIdx.x;
   const int B = s.B, K1 = s.K + 1;
   int b, p, stream, q = -1;
@@ -454,31 +460,29 @@ __global__ void draft_rows_kernel(StepState s, const T* E, int level, T* tri_in,
     kvoff[r] = valid ? enc_off(s, b, stream, p) : -1;
     qrow[r] = q;
   }
-  T* dst = tri_in + (int64_t)r * 3 * s.d;
   if (want_tri && valid) {
-    trigram_row<T>(s, E, b, p, dst);
+    trigram_row<T>(s, E, b, p, tri_in, tri_mtiles, r);
   } else {
-    for (int i = threadIdx.x; i < 3 * s.d; i += blockDim.x) dst[i] = ET<T>::from_f(0.f);
+    for (int i = threadIdx.x; i < 3 * s.d; i += blockDim.x) copy_tiled<T>(tri_in, tri_mtiles, r, i, ET<T>::from_f(0.f));
   }
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void draft_finish_kernel(StepState s, const float* x, const float* parts,
-                                                           int n_parts, T* zin) {
+                                                           int n_parts, T* zin, int z_mtiles) {
   const int b = blockIdx.x, d = s.d;
   const T* hl = (const T*)s.h_last + (int64_t)b * d;
-  T* z = zin + (int64_t)b * 2 * d;
   for (int i = threadIdx.x; i < d; i += 256) {
-    z[i] = hl[i];
+    copy_tiled<T>(zin, z_mtiles, b, i, hl[i]);
     float f = parts[(int64_t)b * d + i];
     for (int q = 1; q < n_parts; ++q) f = f + parts[((int64_t)q * s.B + b) * d + i];
-    z[d + i] = ET<T>::from_f(x[(int64_t)b * d + i] + f);
+    store_tiled<T>(zin, z_mtiles, b, d + i, x[(int64_t)b * d + i] + f);
   }
 }
 
 template <typename T>
 __global__ void prefill_rows_kernel(StepState s, const T* E, int b, int p0, int M, int* tokens_out, T* tri_in,
-                                    int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n) {
+                                    int tri_mtiles, int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n) {
   const int i = blockIdx.x;
   const int p = p0 + i;
   if (threadIdx.x == 0) {
@@ -495,7 +499,7 @@ __global__ void prefill_rows_kernel(StepState s, const T* E, int b, int p0, int 
     enc_qrow[M + i] = -1;
     if (i == 0) pf_n[0] = p0;  // committed length seen by the chunk's attention
   }
-  trigram_row<T>(s, E, b, p, tri_in + (int64_t)i * 3 * s.d);
+  trigram_row<T>(s, E, b, p, tri_in, tri_mtiles, i);
 }
 
 template <typename T>
@@ -520,34 +524,37 @@ void launch_embed(int dtype, const int* tokens, const void* E, float* x, int M, 
 }
 
 template <typename T, int NV>
-static void norm_go(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, int M, int d,
-                    float eps, int write_back, const void* alt, int alt_begin, int alt_end, hipStream_t st) {
-  hipLaunchKernelGGL((rmsnorm_kernel<T, NV>), dim3(M), dim3(256), 0, st, x, parts, n_parts, gamma, (T*)out, ldo, M, d,
-                     eps, write_back, (const T*)alt, alt_begin, alt_end);
+static void norm_go(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, void* out_rm,
+                    int M, int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end,
+                    hipStream_t st) {
+  hipLaunchKernelGGL((rmsnorm_kernel<T, NV>), dim3(M), dim3(256), 0, st, x, parts, n_parts, gamma, (T*)out, ldo,
+                     (T*)out_rm, M, d, eps, write_back, (const T*)alt, alt_begin, alt_end);
 }
 
 template <typename T>
-static void norm_t(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, int M, int d,
-                   float eps, int write_back, const void* alt, int alt_begin, int alt_end, hipStream_t st) {
+static void norm_t(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, void* out_rm,
+                   int M, int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end,
+                   hipStream_t st) {
   switch ((d + 1023) / 1024) {
-    case 1: norm_go<T, 1>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 2: norm_go<T, 2>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 3: norm_go<T, 3>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 4: norm_go<T, 4>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 5: norm_go<T, 5>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 6: norm_go<T, 6>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 7: norm_go<T, 7>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    default: norm_go<T, 8>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 1: norm_go<T, 1>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 2: norm_go<T, 2>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 3: norm_go<T, 3>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 4: norm_go<T, 4>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 5: norm_go<T, 5>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 6: norm_go<T, 6>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    case 7: norm_go<T, 7>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    default: norm_go<T, 8>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
   }
 }
 
-void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, int M,
-                    int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end, hipStream_t st) {
+void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo,
+                    void* out_rm, int M, int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end,
+                    hipStream_t st) {
   if (M <= 0) return;
   if (dtype == DT_BF16)
-    norm_t<bf16_t>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st);
+    norm_t<bf16_t>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st);
   else
-    norm_t<float>(x, parts, n_parts, gamma, out, ldo, M, d, eps, write_back, alt, alt_begin, alt_end, st);
+    norm_t<float>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st);
 }
 
 void launch_argmax(const float* logits, int M, int V, int* amax, hipStream_t st) {
@@ -586,33 +593,36 @@ void launch_advance(int dtype, const StepState& s, hipStream_t st) {
     hipLaunchKernelGGL(advance_kernel<float>, dim3(s.B), dim3(256), 0, st, s);
 }
 
-void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int* pos,
-                       int64_t* kvoff, int* qrow, hipStream_t st) {
+void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int tri_mtiles,
+                       int* pos, int64_t* kvoff, int* qrow, hipStream_t st) {
   const int rows = level == 0 ? s.B * (2 * (s.K + 1) + 1) : s.B;
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(draft_rows_kernel<bf16_t>, dim3(rows), dim3(256), 0, st, s, (const bf16_t*)E, level,
-                       (bf16_t*)tri_in, pos, kvoff, qrow);
+                       (bf16_t*)tri_in, tri_mtiles, pos, kvoff, qrow);
   else
     hipLaunchKernelGGL(draft_rows_kernel<float>, dim3(rows), dim3(256), 0, st, s, (const float*)E, level,
-                       (float*)tri_in, pos, kvoff, qrow);
+                       (float*)tri_in, tri_mtiles, pos, kvoff, qrow);
 }
 
 void launch_draft_finish(int dtype, const StepState& s, const float* x, const float* parts, int n_parts, void* zin,
-                         hipStream_t st) {
+                         int z_mtiles, hipStream_t st) {
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(draft_finish_kernel<bf16_t>, dim3(s.B), dim3(256), 0, st, s, x, parts, n_parts, (bf16_t*)zin);
+    hipLaunchKernelGGL(draft_finish_kernel<bf16_t>, dim3(s.B), dim3(256), 0, st, s, x, parts, n_parts, (bf16_t*)zin,
+                       z_mtiles);
   else
-    hipLaunchKernelGGL(draft_finish_kernel<float>, dim3(s.B), dim3(256), 0, st, s, x, parts, n_parts, (float*)zin);
+    hipLaunchKernelGGL(draft_finish_kernel<float>, dim3(s.B), dim3(256), 0, st, s, x, parts, n_parts, (float*)zin,
+                       z_mtiles);
 }
 
 void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, int p0, int M, int* tokens_out,
-                         void* tri_in, int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n, hipStream_t st) {
+                         void* tri_in, int tri_mtiles, int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n,
+                         hipStream_t st) {
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(prefill_rows_kernel<bf16_t>, dim3(M), dim3(256), 0, st, s, (const bf16_t*)E, b, p0, M,
-                       tokens_out, (bf16_t*)tri_in, enc_pos, enc_kvoff, enc_qrow, pf_n);
+                       tokens_out, (bf16_t*)tri_in, tri_mtiles, enc_pos, enc_kvoff, enc_qrow, pf_n);
   else
     hipLaunchKernelGGL(prefill_rows_kernel<float>, dim3(M), dim3(256), 0, st, s, (const float*)E, b, p0, M, tokens_out,
-                       (float*)tri_in, enc_pos, enc_kvoff, enc_qrow, pf_n);
+                       (float*)tri_in, tri_mtiles, enc_pos, enc_kvoff, enc_qrow, pf_n);
 }
 
 void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,

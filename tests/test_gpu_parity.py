@@ -14,7 +14,7 @@ pytestmark = pytest.mark.gpu
 # GEMM unit (repack + MFMA GEMM), including row-count invariance
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("M,N,K", [(1, 64, 256), (8, 96, 512), (64, 4096, 4096), (100, 1024, 1536), (256, 128, 11008)])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 256), (8, 192, 512), (64, 4096, 4096), (100, 1024, 1536), (256, 128, 11008), (37, 12288, 4096)])
 def test_gemm_matches_fp64(dtype, M, N, K):
     import torch
     from paper_2402_15758_amd import binding as B
