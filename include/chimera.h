@@ -177,6 +177,12 @@ typedef struct {
 chimera_status chimera_profile_enable(chimera_ctx* ctx, int32_t enable);
 chimera_status chimera_profile_read(chimera_ctx* ctx, chimera_profile* out);
 
+/* Launch mode of chimera_step: 1 (default) captures the step's launch
+ * sequence once into a HIP graph and replays it every step (recaptured after
+ * prefill, set_forcing, profile_enable or a stream change; needs a non-null
+ * stream); 0 launches every kernel individually.  Results are identical. */
+chimera_status chimera_set_graph(chimera_ctx* ctx, int32_t enable);
+
 /* Test hook: y[M][N] (float32, host) = x[M][K] @ w[K][N] through the
  * repack and GEMM kernels of `dtype`, on device buffers the call allocates
  * and frees itself.  x and w are host arrays of that dtype. */

@@ -381,9 +381,11 @@ class Decoder:
         return self.pending
 
     # -- draft (Sec. 4.1, Sec. 4.4) ----------------------------------------
-    def draft(self):
+    def draft(self, chain_tokens: Optional[Sequence[int]] = None):
         """Chain drafting: K sequential encoder queries along the rank-0
-        chain.  Returns (level lists [K][s_k], per-head logits [K, V])."""
+        chain.  Returns (level lists [K][s_k], per-head logits [K, V]).
+        ``chain_tokens`` (teacher forcing) replaces each level's rank-0 token
+        as the next chain token, e.g. by another run's choice at a tie."""
         o, n = self.o, self.n
         chain = list(self.seq[: n + 1])  # committed tokens and the pending one
         tri_k, tri_v = self.tri_k, self.tri_v
@@ -402,7 +404,7 @@ class Decoder:
             all_logits.append(z)
             lst = self._select(z, self.s[k], n + 1 + k)
             lists.append(lst)
-            chain.append(lst[0])
+            chain.append(lst[0] if chain_tokens is None else int(chain_tokens[k]))
         return lists, (np.stack(all_logits) if all_logits else np.zeros((0, o.cfg.vocab)))
 
     def _select(self, z: np.ndarray, s: int, j: int) -> List[int]:

@@ -60,6 +60,7 @@ _PROTOS = {
     "chimera_debug_copy": [P, I32, P, I64],
     "chimera_kv_read": [P, I32, I32, I32, I32, P, P],
     "chimera_profile_enable": [P, I32],
+    "chimera_set_graph": [P, I32],
     "chimera_profile_read": [P, ctypes.POINTER(chimera_profile)],
     "chimera_debug_gemm": [I32, P, P, I32, I32, I32, ctypes.POINTER(ctypes.c_float)],
 }
@@ -167,6 +168,10 @@ def chimera_kv_read(kv: int, layer: int, b: int, pos0: int, count: int, k_ptr: i
 
 def chimera_profile_enable(ctx: int, enable: bool):
     _check(lib().chimera_profile_enable(ctx, 1 if enable else 0))
+
+
+def chimera_set_graph(ctx: int, enable: bool):
+    _check(lib().chimera_set_graph(ctx, 1 if enable else 0))
 
 
 def chimera_profile_read(ctx: int) -> chimera_profile:

@@ -217,6 +217,13 @@ struct chimera_ctx {
   hipEvent_t e_start{}, e_draft{}, e_verify{}, e_end{};
   bool ev_created = false;
   chimera_profile acc{};
+  // the step as a HIP graph, replayed every step
+  bool graph_on = true;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  bool graph_prof = false;
+  hipStream_t graph_stream = nullptr;
+  size_t graph_ev_used = 0;
 };
 
 namespace {
@@ -517,6 +524,13 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
     g.run(c->ak, c->mt_b, B, m->head_theta[k], V, d, et);
     launch_topk(c->dlogits, s, k, c->topk_v, c->topk_i, st);
   }
+}
+
+void drop_graph(chimera_ctx* c) {
+  if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
+  if (c->graph) (void)hipGraphDestroy(c->graph);
+  c->gexec = nullptr;
+  c->graph = nullptr;
 }
 
 void check_ctx(chimera_ctx* c) {
@@ -1005,6 +1019,7 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
     }
     hipStream_t st = (hipStream_t)stream;
     ctx->batch = batch;
+    drop_graph(ctx);
     StepState s = make_state(ctx);
     const int dt = m->dt, d = cf.d_model, H = cf.n_heads, hd = cf.head_dim, V = cf.vocab;
     const int hdim = H * hd;
@@ -1087,43 +1102,67 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
     const chimera_config& cf = m->cfg;
     const int dt = m->dt, d = cf.d_model, V = cf.vocab;
     StepState s = make_state(ctx);
-    const Gemm g{ctx, st, true};
-    if (ctx->prof) {
-      if (!ctx->ev_created) {
-        HIPCK(hipEventCreate(&ctx->e_start));
-        HIPCK(hipEventCreate(&ctx->e_draft));
-        HIPCK(hipEventCreate(&ctx->e_verify));
-        HIPCK(hipEventCreate(&ctx->e_end));
-        ctx->ev_pool.resize(1024);
-        ctx->ev_bytes.assign(1024, 0.0);
-        for (auto& e : ctx->ev_pool) {
-          HIPCK(hipEventCreate(&e.a));
-          HIPCK(hipEventCreate(&e.b));
-        }
-        ctx->ev_created = true;
+    if (ctx->prof && !ctx->ev_created) {
+      HIPCK(hipEventCreate(&ctx->e_start));
+      HIPCK(hipEventCreate(&ctx->e_draft));
+      HIPCK(hipEventCreate(&ctx->e_verify));
+      HIPCK(hipEventCreate(&ctx->e_end));
+      ctx->ev_pool.resize(1024);
+      ctx->ev_bytes.assign(1024, 0.0);
+      for (auto& e : ctx->ev_pool) {
+        HIPCK(hipEventCreate(&e.a));
+        HIPCK(hipEventCreate(&e.b));
       }
-      ctx->ev_used = 0;
-      HIPCK(hipEventRecord(ctx->e_start, st));
+      ctx->ev_created = true;
     }
-    if (ctx->K > 0) run_draft(ctx, s, st);
-    if (ctx->prof) HIPCK(hipEventRecord(ctx->e_draft, st));
-    launch_tree_setup(s, st);
-    const int M = ctx->batch * ctx->N;
-    VerifyRows r{ctx->tree_tok, M, ctx->n, kv->page_table, ctx->tree.depth, ctx->tree.path, ctx->N, ctx->D,
-                 ctx->batch};
-    verify_layers(ctx, r, st, true);
-    GemmEpi el;
-    el.kind = EPI_F32;
-    el.out_f = ctx->logits;
-    el.ldo = V;
-    g.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
-    launch_argmax(ctx->logits, M, V, ctx->amax, st);
-    if (ctx->prof) HIPCK(hipEventRecord(ctx->e_verify, st));
-    launch_accept(dt, s, st);
-    launch_compact(dt, s, kv->pool, cf.n_layers, kv->layer_stride, st);
-    launch_advance(dt, s, st);
+    // the launch sequence of one step; every varying scalar lives in device memory
+    auto enqueue = [&](hipStream_t q) {
+      const Gemm gq{ctx, q, true};
+      ctx->ev_used = 0;
+      if (ctx->K > 0) run_draft(ctx, s, q);
+      if (ctx->prof) HIPCK(hipEventRecord(ctx->e_draft, q));
+      launch_tree_setup(s, q);
+      const int M = ctx->batch * ctx->N;
+      VerifyRows r{ctx->tree_tok, M, ctx->n, kv->page_table, ctx->tree.depth, ctx->tree.path, ctx->N, ctx->D,
+                   ctx->batch};
+      verify_layers(ctx, r, q, true);
+      GemmEpi el;
+      el.kind = EPI_F32;
+      el.out_f = ctx->logits;
+      el.ldo = V;
+      gq.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
+      launch_argmax(ctx->logits, M, V, ctx->amax, q);
+      if (ctx->prof) HIPCK(hipEventRecord(ctx->e_verify, q));
+      launch_accept(dt, s, q);
+      launch_compact(dt, s, kv->pool, cf.n_layers, kv->layer_stride, q);
+      launch_advance(dt, s, q);
+    };
+    const bool use_graph = ctx->graph_on && st != nullptr;
+    if (ctx->prof) HIPCK(hipEventRecord(ctx->e_start, st));
+    if (use_graph) {
+      if (ctx->gexec == nullptr || ctx->graph_prof != ctx->prof || ctx->graph_stream != st) {
+        drop_graph(ctx);
+        HIPCK(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+        try {
+          enqueue(st);
+        } catch (...) {
+          hipGraph_t g = nullptr;
+          (void)hipStreamEndCapture(st, &g);
+          if (g) (void)hipGraphDestroy(g);
+          throw;
+        }
+        HIPCK(hipStreamEndCapture(st, &ctx->graph));
+        HIPCK(hipGraphInstantiate(&ctx->gexec, ctx->graph, nullptr, nullptr, 0));
+        ctx->graph_prof = ctx->prof;
+        ctx->graph_stream = st;
+        ctx->graph_ev_used = ctx->ev_used;
+      }
+      ctx->ev_used = ctx->graph_ev_used;
+      HIPCK(hipGraphLaunch(ctx->gexec, st));
+    } else {
+      enqueue(st);
+    }
     if (ctx->prof) HIPCK(hipEventRecord(ctx->e_end, st));
-    HIPCK(hipMemsetAsync(ctx->inject_on, 0, sizeof(int), st));
     HIPCK(hipGetLastError());
     const size_t K1 = ctx->K + 1, B = ctx->batch;
     HIPCK(hipMemcpyAsync(ctx->host_out, ctx->out_tok, sizeof(int) * B * K1, hipMemcpyDeviceToHost, st));
@@ -1162,6 +1201,7 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
 chimera_status chimera_set_forcing(chimera_ctx* ctx, const int32_t* ref, const uint8_t* ok, int32_t stride) {
   return guard([&] {
     check_ctx(ctx);
+    drop_graph(ctx);
     if (ref == nullptr) {
       ctx->f_ref = nullptr;
       ctx->f_ok = nullptr;
@@ -1306,8 +1346,17 @@ chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, i
   });
 }
 
+chimera_status chimera_set_graph(chimera_ctx* ctx, int32_t enable) {
+  return guard([&] {
+    check_ctx(ctx);
+    drop_graph(ctx);
+    ctx->graph_on = enable != 0;
+  });
+}
+
 void chimera_ctx_free(chimera_ctx* ctx) {
   if (!ctx) return;
+  drop_graph(ctx);
   if (ctx->host_out) (void)hipHostFree(ctx->host_out);
   if (ctx->ev_created) {
     (void)hipEventDestroy(ctx->e_start);

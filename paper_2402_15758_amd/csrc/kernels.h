@@ -75,8 +75,8 @@ void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const 
 
 // ---- attention ---------------------------------------------------------------
 // The shared pass of the tree attention writes one partial per group of
-// this many committed positions (4 chunks of 64).
-constexpr int TREE_ATTN_GROUP_POSITIONS = 256;
+// this many committed positions (2 chunks of 64).
+constexpr int TREE_ATTN_GROUP_POSITIONS = 128;
 struct TreeAttnArgs {
   const void* q;            // [B*N][ldq] rotated queries
   int ldq;

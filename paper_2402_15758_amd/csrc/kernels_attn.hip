@@ -7,7 +7,7 @@
 // keys are reduced in 64-position chunks aligned to position 0, in chunk
 // order, with the online softmax:
 //   * chunks 0 .. c_u - 2 (c_u = P_u / 64) hold committed keys only and are
-//     shared by every query of the tree: an MFMA pass over groups of four
+//     shared by every query of the tree: an MFMA pass over groups of two
 //     chunks writes one partial (m, l, O) per group;
 //   * the last two chunks c_u - 1 and c_u, which contain every tree
 //     position, are reduced per query by a VALU pass that first folds the
@@ -265,7 +265,13 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
         const int4 kv = ld16(kr + part * VEC);
         const T* ke = reinterpret_cast<const T*>(&kv);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc = fmaf(q[part * VEC + e], ET<T>::to_f(ke[e]), acc);
+        for (int e4 = 0; e4 < VEC; e4 += 4) {
+          const float4 qv = *reinterpret_cast<const float4*>(q + part * VEC + e4);
+          acc = fmaf(qv.x, ET<T>::to_f(ke[e4 + 0]), acc);
+          acc = fmaf(qv.y, ET<T>::to_f(ke[e4 + 1]), acc);
+          acc = fmaf(qv.z, ET<T>::to_f(ke[e4 + 2]), acc);
+          acc = fmaf(qv.w, ET<T>::to_f(ke[e4 + 3]), acc);
+        }
       }
       s = acc * a.scale;
     }
@@ -283,8 +289,14 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
         const float pi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pe), i));
         const int ri = __builtin_amdgcn_readlane(row, i);
         const T* vr = &Vl[ri * HD + DPL * lane];
+        if constexpr (sizeof(T) == 2 && DPL == 2) {
+          const uint32_t u2 = *reinterpret_cast<const uint32_t*>(vr);
+          o[0] = fmaf(pi, __uint_as_float(u2 << 16), o[0]);
+          o[1] = fmaf(pi, __uint_as_float(u2 & 0xffff0000u), o[1]);
+        } else {
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) o[e] = fmaf(pi, ET<T>::to_f(vr[e]), o[e]);
+          for (int e = 0; e < DPL; ++e) o[e] = fmaf(pi, ET<T>::to_f(vr[e]), o[e]);
+        }
       }
     }
     m = mn;
@@ -310,13 +322,15 @@ void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
 // ---------------------------------------------------------------------------
 // Draft encoder attention: one query per sequence (trigram position n+k)
 // over the target-state entries 0..n-1 and trigram entries 0..n+k.
-// grid (key blocks of 256, H, B); each wave reduces 64 keys.
+// grid (key blocks of 256, H, B); each wave reduces 64 keys, four at a
+// time: lane group sub = lane >> 4 takes key 4*kg + sub and lane c =
+// lane & 15 the head-dim slice [c*HD/16, (c+1)*HD/16).
 // ---------------------------------------------------------------------------
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
+  constexpr int DS = HD / 16;            // dims per lane
   constexpr int VEC = ET<T>::VEC;
-  constexpr int DPL = HD / 64;
-  __shared__ float qs[HD];
+  static_assert(DS % VEC == 0 || VEC % DS == 0, "slice");
   __shared__ float wm[4], wl[4];
   __shared__ float wo[4][HD];
   const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -325,65 +339,80 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
   const int nblk_used = (nkeys + 255) / 256;
   if (blk >= nblk_used) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const T* qrow = (const T*)a.q + (int64_t)b * a.ldq + h * HD;
-  for (int i = tid; i < HD; i += 256) qs[i] = ET<T>::to_f(qrow[i]);
-  __syncthreads();
+  const int sub = lane >> 4, c = lane & 15;
+  float q[DS];
+  {
+    const T* qrow = (const T*)a.q + (int64_t)b * a.ldq + h * HD + c * DS;
+#pragma unroll
+    for (int e = 0; e < DS; ++e) q[e] = ET<T>::to_f(qrow[e]);
+  }
   const int key0 = blk * 256 + wave * 64;
-  const int key = key0 + lane;
-  const bool valid = key < nkeys;
   auto row_ptr = [&](const void* base, int k) -> const T* {
     const int stream = k < n ? 0 : 1;
     const int pos = k < n ? k : k - n;
-    return (const T*)base + ((((int64_t)b * 2 + stream) * a.H + h) * a.cap + pos) * HD;
+    return (const T*)base + ((((int64_t)b * 2 + stream) * a.H + h) * a.cap + pos) * HD + c * DS;
   };
-  float s = -CH_INF;
-  if (valid) {
-    const T* kr = row_ptr(a.kbase, key);
-    float acc = 0.f;
+  float sc[16];
+  float mloc = -CH_INF;
 #pragma unroll
-    for (int part = 0; part < HD / VEC; ++part) {
-      const int4 kv = ld16(kr + part * VEC);
-      const T* ke = reinterpret_cast<const T*>(&kv);
+  for (int kg = 0; kg < 16; ++kg) {
+    const int key = key0 + 4 * kg + sub;
+    float d = 0.f;
+    if (key < nkeys) {
+      const T* kr = row_ptr(a.kbase, key);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) acc = fmaf(qs[part * VEC + e], ET<T>::to_f(ke[e]), acc);
+      for (int e = 0; e < DS; ++e) d = fmaf(q[e], ET<T>::to_f(kr[e]), d);
     }
-    s = acc * a.scale;
+    d = d + __shfl_xor(d, 1);
+    d = d + __shfl_xor(d, 2);
+    d = d + __shfl_xor(d, 4);
+    d = d + __shfl_xor(d, 8);
+    sc[kg] = key < nkeys ? d * a.scale : -CH_INF;
+    mloc = fmaxf(mloc, sc[kg]);
   }
-  const float mw = wave_max(s);
-  const float pe = (valid && mw != -CH_INF) ? expf(s - mw) : 0.f;
-  const float lw = wave_sum(pe);
-  float o[DPL];
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+  const float mw = fmaxf(mloc, __shfl_xor(mloc, 32));
+  float lsum = 0.f, o[DS];
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) o[e] = 0.f;
-  const int cnt = max(0, min(64, nkeys - key0));
-  for (int i = 0; i < cnt; ++i) {
-    const float pi = __shfl(pe, i);
-    const T* vr = row_ptr(a.vbase, key0 + i) + DPL * lane;
+  for (int e = 0; e < DS; ++e) o[e] = 0.f;
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) o[e] = fmaf(pi, ET<T>::to_f(vr[e]), o[e]);
+  for (int kg = 0; kg < 16; ++kg) {
+    const int key = key0 + 4 * kg + sub;
+    const float p = (key < nkeys && mw != -CH_INF) ? expf(sc[kg] - mw) : 0.f;
+    lsum = lsum + p;
+    if (key < nkeys) {
+      const T* vr = row_ptr(a.vbase, key);
+#pragma unroll
+      for (int e = 0; e < DS; ++e) o[e] = fmaf(p, ET<T>::to_f(vr[e]), o[e]);
+    }
+  }
+  lsum = lsum + __shfl_xor(lsum, 16);
+  lsum = lsum + __shfl_xor(lsum, 32);
+#pragma unroll
+  for (int e = 0; e < DS; ++e) {
+    o[e] = o[e] + __shfl_xor(o[e], 16);
+    o[e] = o[e] + __shfl_xor(o[e], 32);
   }
   if (lane == 0) {
     wm[wave] = mw;
-    wl[wave] = lw;
+    wl[wave] = lsum;
   }
+  if (sub == 0) {
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) wo[wave][DPL * lane + e] = o[e];
+    for (int e = 0; e < DS; ++e) wo[wave][c * DS + e] = o[e];
+  }
   __syncthreads();
   if (wave != 0) return;
   float m = -CH_INF;
   for (int w = 0; w < 4; ++w) m = fmaxf(m, wm[w]);
-  float l = 0.f, oo[DPL];
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) oo[e] = 0.f;
-  for (int w = 0; w < 4; ++w) {
-    const float f = exp_diff(wm[w], m);
-    l = l + wl[w] * f;
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) oo[e] = oo[e] + wo[w][DPL * lane + e] * f;
-  }
+  float l = 0.f;
   float* dst = a.part + (((int64_t)b * a.H + h) * a.nblk + blk) * (HD + 2);
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) dst[DPL * lane + e] = oo[e];
+  for (int i = lane; i < HD; i += 64) {
+    float acc = 0.f;
+    for (int w = 0; w < 4; ++w) acc = acc + wo[w][i] * exp_diff(wm[w], m);
+    dst[i] = acc;
+  }
+  for (int w = 0; w < 4; ++w) l = l + wl[w] * exp_diff(wm[w], m);
   if (lane == 0) {
     dst[HD] = m;
     dst[HD + 1] = l;

@@ -16,14 +16,18 @@ __global__ void embed_kernel(const int* __restrict__ tokens, const T* __restrict
   for (int i = threadIdx.x; i < d; i += blockDim.x) x[(int64_t)r * d + i] = ET<T>::to_f(e[i]);
 }
 
-// Fixed-order block sum (256 threads): wave butterflies, then waves in order.
+// Fixed-order block sum: wave butterflies, then the waves in order.
+template <int NW>
 __device__ __forceinline__ float block_sum(float v, float* sh) {
   v = wave_sum(v);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sh[wave] = v;
   __syncthreads();
-  return ((sh[0] + sh[1]) + sh[2]) + sh[3];
+  float t = sh[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) t = t + sh[w];
+  return t;
 }
 
 // 4 consecutive elements of the storage type as floats / back.
@@ -49,22 +53,22 @@ __device__ __forceinline__ void st4f<bf16_t>(bf16_t* p, float4 v) {
   *reinterpret_cast<uint2*>(p) = u;
 }
 
-// One workgroup per row; thread t owns the float4 groups t, t+256, ...
-// (NV of them).  Fixed-order sum of squares.
+// One workgroup of 1024 threads per row; thread t owns the float4 groups
+// t, t+1024, ... (NV of them).  Fixed-order sum of squares.
 template <typename T, int NV>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ parts,
+__global__ __launch_bounds__(1024) void rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ parts,
                                                       int n_parts, const float* __restrict__ gamma, T* __restrict__ out,
                                                       int o_mtiles, T* __restrict__ out_rm, int M, int d, float eps,
                                                       int write_back, const T* __restrict__ alt, int alt_begin,
                                                       int alt_end) {
-  __shared__ float sh[4];
+  __shared__ float sh[16];
   const int r = blockIdx.x;
   const bool use_alt = alt != nullptr && r >= alt_begin && r < alt_end;
   float4 v[NV];
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
-    const int i = 4 * (threadIdx.x + 256 * j);
+    const int i = 4 * (threadIdx.x + 1024 * j);
     float4 val = float4{0.f, 0.f, 0.f, 0.f};
     if (i < d) {
       if (use_alt) {
@@ -94,11 +98,11 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, con
     ss = fmaf(val.z, val.z, ss);
     ss = fmaf(val.w, val.w, ss);
   }
-  ss = block_sum(ss, sh);
+  ss = block_sum<16>(ss, sh);
   const float rinv = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
-    const int i = 4 * (threadIdx.x + 256 * j);
+    const int i = 4 * (threadIdx.x + 1024 * j);
     if (i < d) {
       const float4 gm = *reinterpret_cast<const float4*>(gamma + i);
       float4 o;
@@ -405,6 +409,7 @@ __global__ __launch_bounds__(256) void advance_kernel(StepState s) {
     s.pro_base[b] = n;
     s.pro_count[b] = L;
     s.n[b] = n + L;
+    if (b == 0) s.inject_on[0] = 0;  // injected tree tokens apply to one step only
   }
 }
 
@@ -414,7 +419,7 @@ template <typename T>
 __device__ __forceinline__ void trigram_row(const StepState& s, const T* E, int b, int pos, T* dst, int mtiles,
                                             int row) {
   const int d = s.d;
-  for (int i = threadIdx.x; i < 3 * d; i += blockDim.x) {
+  for (int i = blockIdx.y * blockDim.x + threadIdx.x; i < 3 * d; i += gridDim.y * blockDim.x) {
     const int part = i / d, col = i % d;
     const int p = pos - 2 + part;
     T v = ET<T>::from_f(0.f);
@@ -455,7 +460,7 @@ __global__ void draft_rows_kernel(StepState s, const T* E, int level, T* tri_in,
     p = s.pro_base[b] + e;
     stream = 1;
   }
-  if (threadIdx.x == 0) {
+  if (threadIdx.x == 0 && blockIdx.y == 0) {
     pos[r] = valid ? p : 0;
     kvoff[r] = valid ? enc_off(s, b, stream, p) : -1;
     qrow[r] = q;
@@ -463,7 +468,8 @@ __global__ void draft_rows_kernel(StepState s, const T* E, int level, T* tri_in,
   if (want_tri && valid) {
     trigram_row<T>(s, E, b, p, tri_in, tri_mtiles, r);
   } else {
-    for (int i = threadIdx.x; i < 3 * s.d; i += blockDim.x) copy_tiled<T>(tri_in, tri_mtiles, r, i, ET<T>::from_f(0.f));
+    for (int i = blockIdx.y * blockDim.x + threadIdx.x; i < 3 * s.d; i += gridDim.y * blockDim.x)
+      copy_tiled<T>(tri_in, tri_mtiles, r, i, ET<T>::from_f(0.f));
   }
 }
 
@@ -472,7 +478,7 @@ __global__ __launch_bounds__(256) void draft_finish_kernel(StepState s, const fl
                                                            int n_parts, T* zin, int z_mtiles) {
   const int b = blockIdx.x, d = s.d;
   const T* hl = (const T*)s.h_last + (int64_t)b * d;
-  for (int i = threadIdx.x; i < d; i += 256) {
+  for (int i = blockIdx.y * 256 + threadIdx.x; i < d; i += gridDim.y * 256) {
     copy_tiled<T>(zin, z_mtiles, b, i, hl[i]);
     float f = parts[(int64_t)b * d + i];
     for (int q = 1; q < n_parts; ++q) f = f + parts[((int64_t)q * s.B + b) * d + i];
@@ -527,7 +533,7 @@ template <typename T, int NV>
 static void norm_go(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, void* out_rm,
                     int M, int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end,
                     hipStream_t st) {
-  hipLaunchKernelGGL((rmsnorm_kernel<T, NV>), dim3(M), dim3(256), 0, st, x, parts, n_parts, gamma, (T*)out, ldo,
+  hipLaunchKernelGGL((rmsnorm_kernel<T, NV>), dim3(M), dim3(1024), 0, st, x, parts, n_parts, gamma, (T*)out, ldo,
                      (T*)out_rm, M, d, eps, write_back, (const T*)alt, alt_begin, alt_end);
 }
 
@@ -535,15 +541,9 @@ template <typename T>
 static void norm_t(float* x, const float* parts, int n_parts, const float* gamma, void* out, int ldo, void* out_rm,
                    int M, int d, float eps, int write_back, const void* alt, int alt_begin, int alt_end,
                    hipStream_t st) {
-  switch ((d + 1023) / 1024) {
+  switch ((d + 4095) / 4096) {
     case 1: norm_go<T, 1>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 2: norm_go<T, 2>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 3: norm_go<T, 3>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 4: norm_go<T, 4>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 5: norm_go<T, 5>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 6: norm_go<T, 6>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    case 7: norm_go<T, 7>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
-    default: norm_go<T, 8>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
+    default: norm_go<T, 2>(x, parts, n_parts, gamma, out, ldo, out_rm, M, d, eps, write_back, alt, alt_begin, alt_end, st); break;
   }
 }
 
@@ -596,22 +596,23 @@ void launch_advance(int dtype, const StepState& s, hipStream_t st) {
 void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int tri_mtiles,
                        int* pos, int64_t* kvoff, int* qrow, hipStream_t st) {
   const int rows = level == 0 ? s.B * (2 * (s.K + 1) + 1) : s.B;
+  const dim3 grid(rows, (3 * s.d + 255) / 256);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(draft_rows_kernel<bf16_t>, dim3(rows), dim3(256), 0, st, s, (const bf16_t*)E, level,
+    hipLaunchKernelGGL(draft_rows_kernel<bf16_t>, grid, dim3(256), 0, st, s, (const bf16_t*)E, level,
                        (bf16_t*)tri_in, tri_mtiles, pos, kvoff, qrow);
   else
-    hipLaunchKernelGGL(draft_rows_kernel<float>, dim3(rows), dim3(256), 0, st, s, (const float*)E, level,
+    hipLaunchKernelGGL(draft_rows_kernel<float>, grid, dim3(256), 0, st, s, (const float*)E, level,
                        (float*)tri_in, tri_mtiles, pos, kvoff, qrow);
 }
 
 void launch_draft_finish(int dtype, const StepState& s, const float* x, const float* parts, int n_parts, void* zin,
                          int z_mtiles, hipStream_t st) {
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(draft_finish_kernel<bf16_t>, dim3(s.B), dim3(256), 0, st, s, x, parts, n_parts, (bf16_t*)zin,
-                       z_mtiles);
+    hipLaunchKernelGGL(draft_finish_kernel<bf16_t>, dim3(s.B, (s.d + 255) / 256), dim3(256), 0, st, s, x, parts,
+                       n_parts, (bf16_t*)zin, z_mtiles);
   else
-    hipLaunchKernelGGL(draft_finish_kernel<float>, dim3(s.B), dim3(256), 0, st, s, x, parts, n_parts, (float*)zin,
-                       z_mtiles);
+    hipLaunchKernelGGL(draft_finish_kernel<float>, dim3(s.B, (s.d + 255) / 256), dim3(256), 0, st, s, x, parts,
+                       n_parts, (float*)zin, z_mtiles);
 }
 
 void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, int p0, int M, int* tokens_out,

@@ -153,6 +153,9 @@ class Session:
         B.chimera_kv_read(self.kv, layer, b, pos0, count, k.ctypes.data, v.ctypes.data)
         return k, v
 
+    def set_graph(self, enable: bool):
+        B.chimera_set_graph(self.ctx, enable)
+
     def profile(self, enable: bool):
         B.chimera_profile_enable(self.ctx, enable)
 

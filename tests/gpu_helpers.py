@@ -71,7 +71,9 @@ def check_step(art, b: int, dec: oracle.Decoder, t: float, ties: TieLog, forced=
     tree_g = art["tree"][b]
     logits_g = art["logits"][b]
     if dec.K:
-        lists_o, dz = dec.draft()
+        # the oracle's draft chain follows the GPU's rank-0 tokens (each checked
+        # against the oracle's own list below, with the tie rule)
+        lists_o, dz = dec.draft(chain_tokens=[int(art["lists"][b, k, 0]) for k in range(dec.K)])
         for k in range(dec.K):
             ff = forced is not None and bool(forced.ok[dec.n + 1 + k])
             compare_lists(art["lists"][b, k, : dec.s[k]], lists_o[k], dz[k], t, ties, ff)

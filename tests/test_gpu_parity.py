@@ -274,3 +274,28 @@ def test_small_bf16_batch_ragged(small):
             outs[b] += new
     for b in range(3):
         assert outs[b] == out_a[b][: len(outs[b])]
+
+
+def test_small_bf16_graph_equals_eager(small):
+    """The step replayed as a HIP graph gives the same tokens, paths and
+    verify logits as launching every kernel individually, step after step
+    (host work and synchronisation between the replays)."""
+    import torch
+    w, _ = small
+    log("small bf16: graph replay vs eager launches, 12 steps")
+    prompt = synth.make_prompt(80, SMALL.vocab, 91)
+    outs = []
+    for graph in (False, True):
+        sp = make_session(SMALL, w, synth.TREE_T64, max_len=512)
+        sp.set_graph(graph)
+        sp.prefill([prompt])
+        rec = []
+        for _ in range(12):
+            art = gpu_step(sp)
+            rec.append((art["toks"].copy(), art["n"].copy(), art["path"].copy(), art["logits"].copy()))
+            torch.cuda.synchronize()
+        outs.append(rec)
+        sp.close()
+    for (ta, na, pa, la), (tb, nb, pb, lb) in zip(*outs):
+        assert np.array_equal(ta, tb) and np.array_equal(na, nb) and np.array_equal(pa, pb)
+        assert np.array_equal(la.view(np.uint32), lb.view(np.uint32))
