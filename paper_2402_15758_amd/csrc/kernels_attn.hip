@@ -211,14 +211,37 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
   const T* vpool = (const T*)a.vpool;
   const int* ptab = a.page_table + (int64_t)b * a.max_pages;
 
+  // row -> element offset of its K row (page table read once per row)
+  __shared__ int64_t rowbase[ROWS];
   const int nrows_total = nc + a.N;
-  for (int idx = tid; idx < nrows_total * (HD / VEC); idx += 1024) {
-    const int rr = idx / (HD / VEC), part = idx % (HD / VEC);
+  for (int rr = tid; rr < nrows_total; rr += 1024) {
     const int p = rr < nc ? lo + rr : n + (rr - nc);
-    const int dst = rr < nc ? rr : TAIL_ROWS + (rr - nc);
-    const int64_t base = (int64_t)ptab[p / a.ps] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD + part * VEC;
-    st16(&Kl[dst * KP + part * VEC], ld16(kpool + base));
-    st16(&Vl[dst * HD + part * VEC], ld16(vpool + base));
+    rowbase[rr] = (int64_t)ptab[p / a.ps] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD;
+  }
+  __syncthreads();
+  {
+    constexpr int PARTS = HD / VEC;
+    constexpr int UNR = (ROWS * PARTS + 1023) / 1024;  // iterations per thread, all loads issued first
+    int4 kbuf[UNR], vbuf[UNR];
+#pragma unroll
+    for (int t = 0; t < UNR; ++t) {
+      const int idx = tid + 1024 * t;
+      if (idx < nrows_total * PARTS) {
+        const int64_t base = rowbase[idx / PARTS] + (idx % PARTS) * VEC;
+        kbuf[t] = ld16(kpool + base);
+        vbuf[t] = ld16(vpool + base);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < UNR; ++t) {
+      const int idx = tid + 1024 * t;
+      if (idx < nrows_total * PARTS) {
+        const int rr = idx / PARTS, part = idx % PARTS;
+        const int dst = rr < nc ? rr : TAIL_ROWS + (rr - nc);
+        st16(&Kl[dst * KP + part * VEC], kbuf[t]);
+        st16(&Vl[dst * HD + part * VEC], vbuf[t]);
+      }
+    }
   }
   const int u = 16 * blockIdx.x + wave;
   const bool active = u < a.N;
@@ -232,23 +255,37 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
 
   const int Pu = n + a.depth[u];
   const int cu = Pu / CHUNK;
-  // fold the shared-pass partials in group order
+  // fold the shared-pass partials in group order, loading a batch at a time
   float m = -CH_INF, l = 0.f, o[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) o[e] = 0.f;
   const int lim = cu - 2;
   const int ngrp = lim >= 0 ? lim / GROUP + 1 : 0;
-  for (int gi = 0; gi < ngrp; ++gi) {
-    const int64_t slot = (((int64_t)b * a.H + h) * a.G + gi) * a.N + u;
-    const float mg = a.part_ml[slot * 2], lg = a.part_ml[slot * 2 + 1];
-    if (mg == -CH_INF) continue;
-    const float mn = fmaxf(m, mg);
-    const float a1 = exp_diff(m, mn), a2 = expf(mg - mn);
-    l = l * a1 + lg * a2;
-    const float* po = a.part_o + slot * HD;
+  constexpr int BATCH = 8;
+  for (int g0 = 0; g0 < ngrp; g0 += BATCH) {
+    float bm[BATCH], bl[BATCH], bo[BATCH][DPL];
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + po[DPL * lane + e] * a2;
-    m = mn;
+    for (int t = 0; t < BATCH; ++t) {
+      bm[t] = -CH_INF;
+      bl[t] = 0.f;
+      if (g0 + t < ngrp) {
+        const int64_t slot = (((int64_t)b * a.H + h) * a.G + g0 + t) * a.N + u;
+        bm[t] = a.part_ml[slot * 2];
+        bl[t] = a.part_ml[slot * 2 + 1];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) bo[t][e] = a.part_o[slot * HD + DPL * lane + e];
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < BATCH; ++t) {
+      if (g0 + t >= ngrp || bm[t] == -CH_INF) continue;
+      const float mn = fmaxf(m, bm[t]);
+      const float a1 = exp_diff(m, mn), a2 = expf(bm[t] - mn);
+      l = l * a1 + bl[t] * a2;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + bo[t][e] * a2;
+      m = mn;
+    }
   }
   // the last two chunks, keys in logical-position order
   for (int c = (cu >= 1 ? cu - 1 : 0); c <= cu; ++c) {
