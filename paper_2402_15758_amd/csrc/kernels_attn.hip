@@ -37,28 +37,35 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   __shared__ __attribute__((aligned(16))) T Ks[CHUNK * KP];
   __shared__ __attribute__((aligned(16))) T Vt[HD * VP];
 
+  __shared__ int64_t pbase[GROUP * CHUNK];  // element offset of each staged key's row
   const int grp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int n = a.n_b[b];
-  const int cmax = (n + a.D) / CHUNK;
-  const int last = cmax - 2;            // last chunk any query treats as shared
-  const int c_begin = grp * GROUP;
-  if (c_begin > last) return;
-  const int c_end = min(c_begin + GROUP - 1, last);
-
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
   const int u = 16 * wave + c16;
   const bool wave_on = 16 * wave < a.N;
   const bool valid_u = u < a.N;
   const int uu = valid_u ? u : 0;
-  const int lim_u = (n + a.depth[uu]) / CHUNK - 2;
-
+  // independent loads first: the queries' fragments, their depth, n
   int4 qf[HD / KB];
   if (wave_on) {
     const T* qrow = (const T*)a.q + (int64_t)(b * a.N + uu) * a.ldq + h * HD + g * VEC;
 #pragma unroll
     for (int ks = 0; ks < HD / KB; ++ks) qf[ks] = ld16(qrow + ks * KB);
   }
+  const int dep_u = a.depth[uu];
+  const int n = a.n_b[b];
+  const int cmax = (n + a.D) / CHUNK;
+  const int last = cmax - 2;            // last chunk any query treats as shared
+  const int c_begin = grp * GROUP;
+  if (c_begin > last) return;
+  const int c_end = min(c_begin + GROUP - 1, last);
+  const int lim_u = (n + dep_u) / CHUNK - 2;
+  for (int i = tid; i < (c_end - c_begin + 1) * CHUNK; i += 256) {
+    const int p = c_begin * CHUNK + i;
+    pbase[i] = (int64_t)a.page_table[(int64_t)b * a.max_pages + p / a.ps] * a.page_stride +
+               ((int64_t)h * a.ps + p % a.ps) * HD;
+  }
+  __syncthreads();
   float m = -CH_INF, l = 0.f;
   f32x4 o[HD / 16];
 #pragma unroll
@@ -66,8 +73,6 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 
   const T* kpool = (const T*)a.kpool;
   const T* vpool = (const T*)a.vpool;
-  const int* ptab = a.page_table + (int64_t)b * a.max_pages;
-
   // K rows and V^T of one chunk pass through registers: the global loads of
   // chunk c+1 are issued before chunk c is reduced.
   constexpr int PER = CHUNK * (HD / VEC) / 256;
@@ -77,9 +82,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
     for (int t = 0; t < PER; ++t) {
       const int idx = tid + 256 * t;
       const int key = idx % CHUNK, part = idx / CHUNK;
-      const int p = c * CHUNK + key;
-      const int64_t base =
-          (int64_t)ptab[p / a.ps] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD + part * VEC;
+      const int64_t base = pbase[(c - c_begin) * CHUNK + key] + part * VEC;
       kreg[t] = ld16(kpool + base);
       vreg[t] = ld16(vpool + base);
     }
@@ -188,7 +191,9 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 // ---------------------------------------------------------------------------
 // Tail pass: grid (ceil(N/16), H, B), 16 waves; wave w reduces query
 // 16*blockIdx.x + w.  The committed rows of the last chunks and every tree
-// slot are staged in LDS once per workgroup.
+// slot are staged in LDS once per workgroup.  Loads that do not depend on
+// each other are issued together: (query, n) -> (page offsets, tree paths,
+// first batch of shared-pass partials) -> staged rows.
 // ---------------------------------------------------------------------------
 template <typename T, int HD>
 __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
@@ -196,32 +201,73 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
   constexpr int KP = HD + VEC;
   constexpr int ROWS = TAIL_ROWS + MAX_NODES;
   constexpr int DPL = HD / 64;  // output dims per lane
+  constexpr int PARTS = HD / VEC;
+  constexpr int BATCH = 8;      // shared-pass partials loaded per round trip
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   T* Kl = reinterpret_cast<T*>(smem);
   T* Vl = Kl + ROWS * KP;
   float* qs = reinterpret_cast<float*>(Vl + ROWS * HD);
+  __shared__ int64_t rowbase[ROWS];
+  __shared__ uint8_t spath[16][64];
+  __shared__ int sdepth[16];
 
   const int h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int u = 16 * blockIdx.x + wave;
+  const bool active = u < a.N;
+  // round trip 1: the query row, n, tree metadata of this workgroup's queries
+  T qv[DPL];
+  if (active) {
+    const T* qrow = (const T*)a.q + (int64_t)(b * a.N + u) * a.ldq + h * HD + DPL * lane;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) qv[e] = qrow[e];
+  }
+  for (int i = tid; i < 16 * 64; i += 1024) {
+    const int uu = 16 * blockIdx.x + i / 64;
+    spath[i / 64][i % 64] = uu < a.N ? a.path[uu * 64 + i % 64] : 0;
+  }
+  if (tid < 16) sdepth[tid] = (16 * blockIdx.x + tid) < a.N ? a.depth[16 * blockIdx.x + tid] : 0;
   const int n = a.n_b[b];
   const int cmin = n / CHUNK;
   const int lo = (cmin >= 1 ? cmin - 1 : 0) * CHUNK;  // first staged committed position
   const int nc = n - lo;                               // committed rows staged (<= 127)
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const T* kpool = (const T*)a.kpool;
   const T* vpool = (const T*)a.vpool;
   const int* ptab = a.page_table + (int64_t)b * a.max_pages;
-
-  // row -> element offset of its K row (page table read once per row)
-  __shared__ int64_t rowbase[ROWS];
   const int nrows_total = nc + a.N;
+  // round trip 2: page offsets of the staged rows, first batch of partials
   for (int rr = tid; rr < nrows_total; rr += 1024) {
     const int p = rr < nc ? lo + rr : n + (rr - nc);
     rowbase[rr] = (int64_t)ptab[p / a.ps] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD;
   }
+  // groups every query of the tree folds are bounded by those of the deepest node
+  const int ngrp_max = ((n + a.D) / CHUNK - 2) >= 0 ? ((n + a.D) / CHUNK - 2) / GROUP + 1 : 0;
+  float bm[BATCH], bl[BATCH], bo[BATCH][DPL];
+  auto load_batch = [&](int g0) {
+#pragma unroll
+    for (int t = 0; t < BATCH; ++t) {
+      bm[t] = -CH_INF;
+      bl[t] = 0.f;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) bo[t][e] = 0.f;
+      if (active && g0 + t < ngrp_max) {
+        const int64_t slot = (((int64_t)b * a.H + h) * a.G + g0 + t) * a.N + u;
+        bm[t] = a.part_ml[slot * 2];
+        bl[t] = a.part_ml[slot * 2 + 1];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) bo[t][e] = a.part_o[slot * HD + DPL * lane + e];
+      }
+    }
+  };
+  load_batch(0);
+  if (active) {
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) qs[wave * HD + DPL * lane + e] = ET<T>::to_f(qv[e]);
+  }
   __syncthreads();
+  // round trip 3: the staged rows
   {
-    constexpr int PARTS = HD / VEC;
-    constexpr int UNR = (ROWS * PARTS + 1023) / 1024;  // iterations per thread, all loads issued first
+    constexpr int UNR = (ROWS * PARTS + 1023) / 1024;
     int4 kbuf[UNR], vbuf[UNR];
 #pragma unroll
     for (int t = 0; t < UNR; ++t) {
@@ -243,39 +289,20 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
       }
     }
   }
-  const int u = 16 * blockIdx.x + wave;
-  const bool active = u < a.N;
-  float* q = qs + wave * HD;
-  if (active) {
-    const T* qrow = (const T*)a.q + (int64_t)(b * a.N + u) * a.ldq + h * HD;
-    for (int i = lane; i < HD; i += 64) q[i] = ET<T>::to_f(qrow[i]);
-  }
   __syncthreads();
   if (!active) return;
 
-  const int Pu = n + a.depth[u];
+  const float* q = qs + wave * HD;
+  const int Pu = n + sdepth[wave];
   const int cu = Pu / CHUNK;
-  // fold the shared-pass partials in group order, loading a batch at a time
+  // fold the shared-pass partials in group order
   float m = -CH_INF, l = 0.f, o[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) o[e] = 0.f;
   const int lim = cu - 2;
   const int ngrp = lim >= 0 ? lim / GROUP + 1 : 0;
-  constexpr int BATCH = 8;
   for (int g0 = 0; g0 < ngrp; g0 += BATCH) {
-    float bm[BATCH], bl[BATCH], bo[BATCH][DPL];
-#pragma unroll
-    for (int t = 0; t < BATCH; ++t) {
-      bm[t] = -CH_INF;
-      bl[t] = 0.f;
-      if (g0 + t < ngrp) {
-        const int64_t slot = (((int64_t)b * a.H + h) * a.G + g0 + t) * a.N + u;
-        bm[t] = a.part_ml[slot * 2];
-        bl[t] = a.part_ml[slot * 2 + 1];
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) bo[t][e] = a.part_o[slot * HD + DPL * lane + e];
-      }
-    }
+    if (g0 > 0) load_batch(g0);
 #pragma unroll
     for (int t = 0; t < BATCH; ++t) {
       if (g0 + t >= ngrp || bm[t] == -CH_INF) continue;
@@ -294,20 +321,20 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
     int row = 0;
     float s = -CH_INF;
     if (valid) {
-      row = p < n ? p - lo : TAIL_ROWS + (int)a.path[u * 64 + (p - n)];
+      row = p < n ? p - lo : TAIL_ROWS + (int)spath[wave][p - n];
       const T* kr = &Kl[row * KP];
       float acc = 0.f;
 #pragma unroll
-      for (int part = 0; part < HD / VEC; ++part) {
+      for (int part = 0; part < PARTS; ++part) {
         const int4 kv = ld16(kr + part * VEC);
         const T* ke = reinterpret_cast<const T*>(&kv);
 #pragma unroll
         for (int e4 = 0; e4 < VEC; e4 += 4) {
-          const float4 qv = *reinterpret_cast<const float4*>(q + part * VEC + e4);
-          acc = fmaf(qv.x, ET<T>::to_f(ke[e4 + 0]), acc);
-          acc = fmaf(qv.y, ET<T>::to_f(ke[e4 + 1]), acc);
-          acc = fmaf(qv.z, ET<T>::to_f(ke[e4 + 2]), acc);
-          acc = fmaf(qv.w, ET<T>::to_f(ke[e4 + 3]), acc);
+          const float4 qq = *reinterpret_cast<const float4*>(q + part * VEC + e4);
+          acc = fmaf(qq.x, ET<T>::to_f(ke[e4 + 0]), acc);
+          acc = fmaf(qq.y, ET<T>::to_f(ke[e4 + 1]), acc);
+          acc = fmaf(qq.z, ET<T>::to_f(ke[e4 + 2]), acc);
+          acc = fmaf(qq.w, ET<T>::to_f(ke[e4 + 3]), acc);
         }
       }
       s = acc * a.scale;

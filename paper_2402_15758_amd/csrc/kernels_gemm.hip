@@ -21,6 +21,11 @@ namespace {
 
 constexpr int NB = 4;  // 16-column blocks per weight-layout group
 constexpr int PF = 2;  // k-blocks in flight per wave
+// Matrices at least this wide run unsplit (their epilogue needs whole sums and
+// they already have >= 128 column groups); narrower ones split the reduction
+// until a launch has at least SPLIT_TARGET_WGS workgroups.
+constexpr int SPLIT_MIN_COLS_NO = 8192;
+constexpr int SPLIT_TARGET_WGS = 256;
 
 // ---------------------------------------------------------------------------
 // Weight repacking (load time)
@@ -289,10 +294,10 @@ int gemm_pick_splits(int n_cols, int K, int dtype) {
   // narrow ones split the reduction so that >= 256 workgroups stream weights.
   const int KB = dtype == DT_BF16 ? 32 : 16;
   const int kblocks = K / KB;
-  if (n_cols >= 8192) return 1;
+  if (n_cols >= SPLIT_MIN_COLS_NO) return 1;
   const int groups = n_cols / 64;
   int s = 1;
-  while (groups * s < 256 && s < 8 && kblocks % (2 * s) == 0 && kblocks / (2 * s) >= 16) s *= 2;
+  while (groups * s < SPLIT_TARGET_WGS && s < 8 && kblocks % (2 * s) == 0 && kblocks / (2 * s) >= 16) s *= 2;
   return s;
 }
 
