@@ -45,7 +45,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama7b_p512")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-ar", action="store_true", help="skip timing the greedy-decoding rate")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -196,6 +197,14 @@ def main():
         f"verify {prof.ms_verify / prof.steps:.3f} ms ({verify_gbs:.0f} GB/s), draft {prof.ms_draft / prof.steps:.3f} ms, "
         f"gemm {gemm_gbs:.0f} GB/s, lossless={lossless}")
 
+    if a.calibrate_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] copy calibration: 3 x 1 GiB device copies")
+        del src, dst
     cpu = None
     if not a.no_cpu_baseline and len(prompts) == 1:
         log("[bench] CPU oracle baseline (bounded sample)")
