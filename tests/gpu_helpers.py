@@ -95,3 +95,67 @@ def check_step(art, b: int, dec: oracle.Decoder, t: float, ties: TieLog, forced=
     assert list(art["toks"][b, :L]) == new_o
     dec.commit(path_o, bonus_o, list(tree_g), h_o, tkv)
     return new_o, err
+
+
+def chain_nodes(tree_ranks):
+    """Node ids of the rank-0 chain (root, then (0,), (0, 0), ...)."""
+    return [0] + [i + 1 for i, r in enumerate(tree_ranks) if all(x == 0 for x in r)]
+
+
+def forced_lossless_run(cfg, weights, wl, steps: int, extra: int = 128):
+    """Run the workload's forced speculative decoding for `steps` steps and
+    check, per sequence, the properties that hold at any size: the stream
+    equals the GPU's greedy stream token for token, and every step accepts
+    exactly 1 + (consecutive seeded successes) tokens along the rank-0
+    chain.  Returns the mean accepted length."""
+    import torch
+    prompts = wl.prompts()
+    tree = synth.TREES[wl.tree]
+    K = max(len(r) for r in tree)
+    B = len(prompts)
+    max_len = max(len(p) for p in prompts) + steps * (K + 1) + extra
+    max_len = (max_len + 63) // 64 * 64
+    log(f"{wl.name}: greedy reference for {B} sequence(s), max_len {max_len}")
+    ar = make_session(cfg, weights, (), max_batch=B, max_len=max_len)
+    n_ref = steps * (K + 1) + K + 2
+    streams = [[int(t)] for t in ar.prefill(prompts)]
+    while min(len(s) for s in streams) < n_ref:
+        toks, n, _ = ar.step()
+        for b in range(B):
+            streams[b] += [int(x) for x in toks[b, : n[b]]]
+    ar.close()
+    stride = max_len + 8
+    ref = np.full((B, stride), -1, dtype=np.int32)
+    ok = np.zeros((B, stride), dtype=np.uint8)
+    ps = wl.accept_probs()
+    for b in range(B):
+        n0 = len(prompts[b])
+        a = streams[b][: stride - n0]
+        ref[b, n0:n0 + len(a)] = a
+        ok[b] = synth.force_table(ps[b], wl.force_seed, b, stride)
+    log(f"{wl.name}: {steps} forced speculative steps, tree {wl.tree}")
+    sp = make_session(cfg, weights, tree, max_batch=B, max_len=max_len)
+    sp.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+    first = sp.prefill(prompts)
+    out = [[int(t)] for t in first]
+    pos = [len(p) for p in prompts]
+    chain = chain_nodes(tree)
+    total = 0
+    for _ in range(steps):
+        toks, nn, path = sp.step()
+        for b in range(B):
+            L = int(nn[b])
+            run = 0
+            while run < K and ok[b, pos[b] + 1 + run]:
+                run += 1
+            assert L == 1 + run, (b, pos[b], L, run)
+            assert list(path[b, :L]) == chain[:L], (b, list(path[b, :L]))
+            out[b] += [int(t) for t in toks[b, :L]]
+            pos[b] += L
+            total += L
+    sp.close()
+    for b in range(B):
+        assert out[b] == streams[b][: len(out[b])], f"sequence {b} differs from greedy decoding"
+    mean = total / (steps * B)
+    log(f"{wl.name}: lossless over {B} x {steps} steps, mean accepted {mean:.2f}")
+    return mean

@@ -6,16 +6,18 @@ benchmark times.
   130-token prompt (two shared attention chunks plus the tail), checked
   node by node against a float32 oracle holding every 7B weight.
 * Properties that hold at any size, on the benchmark workload itself
-  (512-token prompt, forced acceptance p = 0.7): the speculative stream
-  equals the GPU's greedy stream token for token, and every step accepts
-  exactly 1 + (consecutive seeded successes) tokens along the rank-0 chain.
+  (512-token prompt, forced acceptance p = 0.7), on the 4096-token paged
+  context and on the ragged batch of 8 (prompts U[256, 2048], T32,
+  p_b ~ U[0.4, 0.9]): the speculative stream equals the GPU's greedy stream
+  token for token, and every step accepts exactly 1 + (consecutive seeded
+  successes) tokens along the rank-0 chain.
 """
 import numpy as np
 import pytest
 
 import oracle
 import synth
-from gpu_helpers import TieLog, check_step, gpu_step, log, make_session, tau
+from gpu_helpers import TieLog, check_step, forced_lossless_run, gpu_step, log, make_session, tau
 
 pytestmark = pytest.mark.gpu
 
@@ -84,3 +86,11 @@ def test_llama7b_p512_lossless_and_forced_acceptance(w7b):
     assert out == out_a[0][: len(out)]
     log(f"llama7b_p512: {len(out)} tokens lossless, mean accepted {len(out) / steps:.2f}")
     sp.close()
+
+
+def test_llama7b_p4096_lossless_and_forced_acceptance(w7b):
+    forced_lossless_run(CFG, w7b, synth.WORKLOADS["llama7b_p4096"], steps=16)
+
+
+def test_llama7b_batch8_ragged_lossless_and_forced_acceptance(w7b):
+    forced_lossless_run(CFG, w7b, synth.WORKLOADS["llama7b_b8"], steps=16)
