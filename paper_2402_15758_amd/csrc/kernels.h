@@ -12,11 +12,11 @@ enum { DT_F32 = 0, DT_BF16 = 1 };
 // W[kb KB + (l >> 4) VEC + e][16 nb + (l & 15)], e < VEC.  Tiles of one
 // column block are contiguous along kb, so a workgroup streams them linearly.
 enum { PACK_NATURAL = 0, PACK_QKV = 1, PACK_GU = 2 };
-// PACK_QKV interleaves, per head, the two halves of each rotary pair so that
-// packed column blocks 2p and 2p+1 hold dims [16p', 16p'+16) and
-// [hd/2 + 16p', ...) of the same head (V keeps its natural order);
-// PACK_GU interleaves gate and up: blocks 2p / 2p+1 = gate / up columns
-// [16p, 16p+16).
+// PACK_QKV puts both halves of 8 rotary pairs in one 16-column block: for
+// Q and K, block q of a head holds dims 8q + l (lane column l < 8) and
+// hd/2 + 8q + l - 8 (l >= 8); V keeps its natural order.  PACK_GU puts gate
+// columns 8c + l (l < 8) and up columns 8c + l - 8 (l >= 8) in block c.  The
+// epilogue pairs lane columns l and l ^ 8.
 
 enum { EPI_F32 = 0, EPI_T = 1, EPI_SILU = 2, EPI_SWIGLU = 3, EPI_QKV = 4, EPI_PARTIAL = 5 };
 
@@ -50,8 +50,8 @@ struct GemmShape {
   const void* W = nullptr;  // packed
   int N = 0;                // packed columns of the whole matrix
   int K = 0;
-  int nb_off = 0;           // first 16-column block to compute (multiple of 4)
-  int nb_count = 0;         // number of 16-column blocks to compute (multiple of 4); 0 = all
+  int nb_off = 0;           // first 16-column block to compute
+  int nb_count = 0;         // number of 16-column blocks to compute; 0 = all
   int splits = 1;           // split of the reduction across workgroups
 };
 

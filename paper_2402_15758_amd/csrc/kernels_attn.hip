@@ -39,7 +39,8 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 
   __shared__ int64_t pbase[GROUP * CHUNK];  // element offset of each staged key's row
   const int grp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave-uniform wave index: the MFMAs below sit under wave-level branches only
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
   const int u = 16 * wave + c16;
   const bool wave_on = 16 * wave < a.N;

@@ -3,32 +3,47 @@
 //
 // Both operands are stored in MFMA fragment order, so every operand load of
 // a wave is one contiguous 1 KiB (64 lanes x 16 bytes):
-//   * W (repacked at load): workgroup column group g (4 blocks of 16
-//     columns) stores its tiles as [g][kb][4][1 KiB];
+//   * W (repacked at load): layout group g of 4 column blocks stores its
+//     tiles as [g][kb][4][1 KiB];
 //   * X (written tiled by the kernel that produces it): tile (kb, mb) of
 //     16 rows x KB reduction indices at ((kb * mtiles + mb) * 64 + lane).
-// A workgroup = 4 wave64s owns CB column blocks (64 columns; 32 for
-// single-tile launches) and one slice of the reduction (split-K across
-// workgroups); its waves take interleaved k-blocks and are summed through
-// LDS in wave order.  Split-K slices are written as partials and summed in
+//
+// Work split.  A launch runs GEMM_WGS / splits workgroups per reduction slice
+// (more only when a matrix has over CB_MAX column blocks per workgroup), and
+// the 16-column blocks are dealt out in contiguous runs whose lengths differ
+// by at most one, so every CU streams the same number of weight bytes and
+// the activation tiles a workgroup reads are reused across its whole run.
+// A workgroup = 4 wave64s; its waves take interleaved k-blocks and are summed
+// through LDS in wave order.  The steady-state loop issues the loads of
+// stage s + PF unconditionally, so the wait before stage s only covers that
+// stage's own loads.  Split-K slices are written as partials and summed in
 // slice order by their consumer (the next norm) or by a finishing pass that
 // applies the epilogue.  Every row's arithmetic depends only on (N, K): the
-// same row gives identical bits whether a launch carries 1 or 64 rows.
+// same row gives identical bits whether a launch carries 1 or 256 rows.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace {
 
-constexpr int NB = 4;  // 16-column blocks per weight-layout group
-constexpr int PF = 2;  // k-blocks in flight per wave
+constexpr int NB = 4;        // 16-column blocks per weight-layout group
+constexpr int CB_MAX = 8;    // column blocks per workgroup, upper bound
+constexpr int GEMM_WGS = 256;  // one workgroup per CU per reduction slice
 // Matrices at least this wide run unsplit (their epilogue needs whole sums and
-// they already have >= 128 column groups); narrower ones split the reduction
-// until a launch has at least SPLIT_TARGET_WGS workgroups.
+// they fill the GPU on their own); narrower ones split the reduction until a
+// launch has at least SPLIT_TARGET_WGS 64-column groups' worth of work.
 constexpr int SPLIT_MIN_COLS_NO = 8192;
 constexpr int SPLIT_TARGET_WGS = 256;
 
 // ---------------------------------------------------------------------------
-// Weight repacking (load time)
+// Weight repacking (load time).  Packed column block c, lane column cl:
+//   PACK_NATURAL: column 16 c + cl.
+//   PACK_QKV: sections Q, K, V of H * hd / 16 blocks each; block q of head h
+//     holds, for Q and K, rotary dims 8q + cl (cl < 8) and hd/2 + 8q + cl - 8
+//     (cl >= 8), so both halves of a rotary pair sit in lanes cl and cl ^ 8;
+//     V keeps dims 16q + cl.
+//   PACK_GU: gate column 8c + cl (cl < 8) and up column 8c + cl - 8 (cl >= 8).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void repack_kernel(const T* __restrict__ s0, const T* __restrict__ s1, const T* __restrict__ s2, int K,
@@ -48,13 +63,13 @@ __global__ void repack_kernel(const T* __restrict__ s0, const T* __restrict__ s1
   if (kind == PACK_QKV) {
     const int per_sec = H * hd / 16;
     const int sec = c / per_sec, within = c % per_sec;
-    const int h = within / (hd / 16), blk = within % (hd / 16);
-    const int dim = sec < 2 ? (blk & 1) * (hd / 2) + 16 * (blk >> 1) + cl : 16 * blk + cl;
+    const int h = within / (hd / 16), q = within % (hd / 16);
+    const int dim = sec < 2 ? (cl < 8 ? 8 * q + cl : hd / 2 + 8 * q + cl - 8) : 16 * q + cl;
     src = sec == 0 ? s0 : (sec == 1 ? s1 : s2);
     col = h * hd + dim;
   } else if (kind == PACK_GU) {
-    src = (c & 1) ? s1 : s0;
-    col = 16 * (c >> 1) + cl;
+    src = cl < 8 ? s0 : s1;
+    col = 8 * c + (cl & 7);
   } else {
     col = 16 * c + cl;
   }
@@ -65,63 +80,49 @@ __global__ void repack_kernel(const T* __restrict__ s0, const T* __restrict__ s1
 }
 
 // ---------------------------------------------------------------------------
-// Epilogue on one column pair: (v0, v1) are the values of packed column
-// blocks 2*pair and 2*pair+1 at column offset c16 of row `row`.
+// Epilogue of one output element: v is packed column 16 blk + c16 of `row`,
+// vp the same row's value at lane column c16 ^ 8 (the other half of a rotary
+// or gate/up pair).
 // ---------------------------------------------------------------------------
-template <typename T, int EPI>
-__device__ __forceinline__ void epi_pair(const GemmEpi& e, int N, int M, int split, int row, int pair, int c16,
-                                         float v0, float v1) {
-  if constexpr (EPI == EPI_PARTIAL) {
-    float* p = e.part + ((int64_t)split * M + row) * N + 32 * pair + c16;
-    p[0] = v0;
-    p[16] = v1;
-  } else if constexpr (EPI == EPI_F32) {
-    float* p = e.out_f + (int64_t)row * e.ldo + 32 * pair + c16;
-    p[0] = v0;
-    p[16] = v1;
-  } else if constexpr (EPI == EPI_T) {
-    store_tiled<T>((T*)e.out_t, e.o_mtiles, row, 32 * pair + c16, v0);
-    store_tiled<T>((T*)e.out_t, e.o_mtiles, row, 32 * pair + 16 + c16, v1);
-  } else if constexpr (EPI == EPI_SILU) {
-    store_tiled<T>((T*)e.out_t, e.o_mtiles, row, 32 * pair + c16, silu_f(v0));
-    store_tiled<T>((T*)e.out_t, e.o_mtiles, row, 32 * pair + 16 + c16, silu_f(v1));
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    store_tiled<T>((T*)e.out_t, e.o_mtiles, row, 16 * pair + c16, silu_f(v0) * v1);
-  } else if constexpr (EPI == EPI_QKV) {
+template <typename T>
+__device__ __forceinline__ void epi_elem(const GemmEpi& e, int kind, int N, int M, int split, int row, int blk,
+                                         int c16, float v, float vp) {
+  const int col = 16 * blk + c16;
+  if (kind == EPI_PARTIAL) {
+    e.part[((int64_t)split * M + row) * N + col] = v;
+  } else if (kind == EPI_F32) {
+    e.out_f[(int64_t)row * e.ldo + col] = v;
+  } else if (kind == EPI_T) {
+    store_tiled<T>((T*)e.out_t, e.o_mtiles, row, col, v);
+  } else if (kind == EPI_SILU) {
+    store_tiled<T>((T*)e.out_t, e.o_mtiles, row, col, silu_f(v));
+  } else if (kind == EPI_SWIGLU) {
+    if (c16 < 8) store_tiled<T>((T*)e.out_t, e.o_mtiles, row, 8 * blk + c16, silu_f(v) * vp);
+  } else if (kind == EPI_QKV) {
     const int hd = e.hd;
-    const int pairs_head = hd / 32;
-    const int sec_pairs = e.H * pairs_head;
-    const int sec = pair / sec_pairs, rem = pair % sec_pairs;
-    const int h = rem / pairs_head, pp = rem % pairs_head;
+    const int blk_head = hd / 16;
+    const int sec_blks = e.H * blk_head;
+    const int sec = blk / sec_blks, rem = blk % sec_blks;
+    const int h = rem / blk_head, q = rem % blk_head;
     if (sec < 2) {
-      const int i = 16 * pp + c16;
+      const bool first = c16 < 8;
+      const int i = 8 * q + (c16 & 7);
       const int pos = e.pos[row];
       const float c = e.rcos[(int64_t)pos * (hd / 2) + i];
       const float s = e.rsin[(int64_t)pos * (hd / 2) + i];
-      const float o0 = v0 * c - v1 * s;
-      const float o1 = v1 * c + v0 * s;
+      // first half: x1 cos - x2 sin; second half: x2 cos + x1 sin
+      const float o = first ? v * c - vp * s : v * c + vp * s;
+      const int dim = first ? i : i + hd / 2;
       if (sec == 0) {
         const int qr = e.qrow[row];
-        if (qr >= 0) {
-          T* q = (T*)e.qout + (int64_t)qr * e.ldq + h * hd;
-          q[i] = ET<T>::from_f(o0);
-          q[i + hd / 2] = ET<T>::from_f(o1);
-        }
+        if (qr >= 0) ((T*)e.qout)[(int64_t)qr * e.ldq + h * hd + dim] = ET<T>::from_f(o);
       } else {
         const int64_t off = e.kvoff[row];
-        if (off >= 0) {
-          T* k = (T*)e.kbase + off + h * e.head_stride;
-          k[i] = ET<T>::from_f(o0);
-          k[i + hd / 2] = ET<T>::from_f(o1);
-        }
+        if (off >= 0) ((T*)e.kbase)[off + h * e.head_stride + dim] = ET<T>::from_f(o);
       }
     } else {
       const int64_t off = e.kvoff[row];
-      if (off >= 0) {
-        T* v = (T*)e.vbase + off + h * e.head_stride;
-        v[32 * pp + c16] = ET<T>::from_f(v0);
-        v[32 * pp + 16 + c16] = ET<T>::from_f(v1);
-      }
+      if (off >= 0) ((T*)e.vbase)[off + h * e.head_stride + 16 * q + c16] = ET<T>::from_f(v);
     }
   }
 }
@@ -133,24 +134,27 @@ __device__ __forceinline__ int4 ldw(const T* p) {
   return int4{v.x, v.y, v.z, v.w};
 }
 
-// ---------------------------------------------------------------------------
-// The GEMM.  grid = (column groups of 16*CB, row blocks of 16*MB, splits).
-// ---------------------------------------------------------------------------
-template <typename T, int MB, int CB, int EPI>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const GemmEpi e) {
-  constexpr int VEC = ET<T>::VEC, KB = 4 * VEC;
-  __shared__ f32x4 red[4][MB][CB][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// One workgroup's run of CB column blocks starting at block cb0, rows
+// [16 mb0, 16 (mb0 + MB)), reduction slice [kbeg, kend).  red: LDS of
+// [4][MB][CB][64] f32x4.
+template <typename T, int MB, int CB, int PF>
+__device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0, int kbeg,
+                                         int kend, f32x4* red) {
+  constexpr int VEC = ET<T>::VEC;
+  // The wave index is made provably wave-uniform so that every branch of the
+  // k-loop below is a scalar branch: an MFMA ignores EXEC, so it must never
+  // sit in a lane-predicated region.
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, c16 = lane & 15;
-  const int kblocks = sh.K / KB;
-  const int cb0 = sh.nb_off + blockIdx.x * CB;      // first 16-column block
-  const int grp = cb0 / NB, sub = cb0 % NB;          // layout group, offset inside it
-  const int mb0 = blockIdx.y * MB;
-  const int kps = kblocks / sh.splits;
-  const int kbeg = blockIdx.z * kps;
-  const int kend = kbeg + kps;
+  const int kblocks = sh.K / (4 * VEC);
   const T* X = (const T*)sh.X + (int64_t)lane * VEC;
-  const T* W = (const T*)sh.W + (((int64_t)grp * kblocks * NB + sub) * 64 + lane) * VEC;
+  const T* Wl = (const T*)sh.W + (int64_t)lane * VEC;
+  int64_t wofs[CB];
+#pragma unroll
+  for (int j = 0; j < CB; ++j) {
+    const int c = cb0 + j;
+    wofs[j] = ((int64_t)(c / NB) * kblocks * NB + c % NB) * 64 * VEC;
+  }
 
   f32x4 acc[MB][CB];
 #pragma unroll
@@ -161,113 +165,152 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const Gem
   int4 bw[PF][CB], bx[PF][MB];
   auto load = [&](int s, int kb) {
 #pragma unroll
-    for (int j = 0; j < CB; ++j) bw[s][j] = ldw(W + ((int64_t)kb * NB + j) * 64 * VEC);
+    for (int j = 0; j < CB; ++j) bw[s][j] = ldw(Wl + wofs[j] + (int64_t)kb * NB * 64 * VEC);
 #pragma unroll
     for (int i = 0; i < MB; ++i) bx[s][i] = ld16(X + ((int64_t)kb * sh.x_mtiles + mb0 + i) * 64 * VEC);
   };
-  const int kfirst = kbeg + wave;
+  auto mma = [&](int s) {
 #pragma unroll
-  for (int s = 0; s < PF; ++s)
-    if (kfirst + 4 * s < kend) load(s, kfirst + 4 * s);
-  for (int it = 0;; it += PF) {
-    bool done = false;
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int j = 0; j < CB; ++j) acc[i][j] = mfma_kb<T>(bx[s][i], bw[s][j], acc[i][j]);
+  };
+  // wave w takes k-blocks kbeg + w, kbeg + w + 4, ... (nk of them)
+  const int kfirst = kbeg + wave;
+  const int nk = kfirst < kend ? (kend - kfirst + 3) / 4 : 0;
+  if (nk >= PF) {
+#pragma unroll
+    for (int s = 0; s < PF; ++s) load(s, kfirst + 4 * s);
+    int it = 0;
+    for (; it + 2 * PF <= nk; it += PF) {
+#pragma unroll
+      for (int s = 0; s < PF; ++s) {
+        mma(s);
+        load(s, kfirst + 4 * (it + PF + s));
+      }
+    }
+    // stages it .. it+PF-1 are loaded; rem (< PF) k-blocks remain after them
+    const int rem = nk - it - PF;
 #pragma unroll
     for (int s = 0; s < PF; ++s) {
-      const int kb = kfirst + 4 * (it + s);
-      if (kb >= kend) {
-        done = true;
-        break;
-      }
-#pragma unroll
-      for (int i = 0; i < MB; ++i)
-#pragma unroll
-        for (int j = 0; j < CB; ++j) acc[i][j] = mfma_kb<T>(bx[s][i], bw[s][j], acc[i][j]);
-      const int kn = kb + 4 * PF;
-      if (kn < kend) load(s, kn);
+      mma(s);
+      if (s < rem) load(s, kfirst + 4 * (it + PF + s));
     }
-    if (done) break;
+#pragma unroll
+    for (int s = 0; s < PF - 1; ++s)
+      if (s < rem) mma(s);
+  } else {
+    for (int t = 0; t < nk; ++t) {
+      load(0, kfirst + 4 * t);
+      mma(0);
+    }
   }
 
 #pragma unroll
   for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int j = 0; j < CB; ++j) red[wave][i][j][lane] = acc[i][j];
+    for (int j = 0; j < CB; ++j) red[((wave * MB + i) * CB + j) * 64 + lane] = acc[i][j];
   __syncthreads();
-  constexpr int ITEMS = MB * (CB / 2);
-  for (int it = wave; it < ITEMS; it += 4) {
-    const int i = it / (CB / 2), jp = it % (CB / 2);
-    f32x4 v0 = red[0][i][2 * jp][lane];
-    f32x4 v1 = red[0][i][2 * jp + 1][lane];
+  for (int it = wave; it < MB * CB; it += 4) {
+    const int i = it / CB, j = it % CB;
+    f32x4 v = red[((0 * MB + i) * CB + j) * 64 + lane];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) {
-      v0 = v0 + red[w][i][2 * jp][lane];
-      v1 = v1 + red[w][i][2 * jp + 1][lane];
-    }
-    const int pair = cb0 / 2 + jp;
+    for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * CB + j) * 64 + lane];
+    f32x4 vp;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) vp[r] = __shfl_xor(v[r], 8);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = 16 * (mb0 + i) + 4 * g + r;
-      if (row < sh.M) epi_pair<T, EPI>(e, sh.N, sh.M, blockIdx.z, row, pair, c16, v0[r], v1[r]);
+      if (row < sh.M) epi_elem<T>(e, kind, sh.N, sh.M, blockIdx.z, row, cb0 + j, c16, v[r], vp[r]);
     }
   }
 }
 
-// Sum split-K partials in split order and apply the epilogue.
-template <typename T, int EPI>
-__global__ void gemm_finish_kernel(const GemmShape sh, const GemmEpi e, const float* __restrict__ part) {
-  const int npairs = (sh.nb_count ? sh.nb_count : sh.N / 16) / 2;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)sh.M * npairs * 16;
-  if (tid >= total) return;
-  const int c16 = (int)(tid & 15);
-  const int pr = (int)((tid >> 4) % npairs);
-  const int row = (int)((tid >> 4) / npairs);
-  const int pair = (sh.nb_off >> 1) + pr;
-  float v0 = 0.f, v1 = 0.f;
-  for (int s = 0; s < sh.splits; ++s) {
-    const float* p = part + ((int64_t)s * sh.M + row) * sh.N + 32 * pair + c16;
-    v0 = (s == 0) ? p[0] : v0 + p[0];
-    v1 = (s == 0) ? p[16] : v1 + p[16];
+// grid = (row blocks of 16 MB, workgroups per slice, splits).  Workgroups
+// [0, nbig) own CBA column blocks, the others CBA - 1.
+template <typename T, int MB, int CBA>
+__global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const GemmEpi e, int kind, int nbig) {
+  constexpr int PF = MB == 1 ? 4 : 3;
+  __shared__ f32x4 red[4 * MB * CBA * 64];
+  const int kblocks = sh.K / (4 * ET<T>::VEC);
+  const int kps = kblocks / sh.splits;
+  const int kbeg = blockIdx.z * kps;
+  const int kend = kbeg + kps;
+  const int b = blockIdx.y;
+  const int mb0 = blockIdx.x * MB;
+  if (b < nbig) {
+    gemm_run<T, MB, CBA, PF>(sh, e, kind, sh.nb_off + b * CBA, mb0, kbeg, kend, red);
+  } else {
+    if constexpr (CBA > 1)
+      gemm_run<T, MB, CBA - 1, PF>(sh, e, kind, sh.nb_off + nbig * CBA + (b - nbig) * (CBA - 1), mb0, kbeg, kend,
+                                   red);
   }
-  epi_pair<T, EPI>(e, sh.N, sh.M, 0, row, pair, c16, v0, v1);
 }
 
-template <typename T, int MB, int EPI>
-void gemm_go(const GemmShape& s, const GemmEpi& e, hipStream_t st) {
-  constexpr int CB = MB == 1 ? 2 : 4;
-  const int nbc = s.nb_count ? s.nb_count : s.N / 16;
-  dim3 grid(nbc / CB, (s.M + 16 * MB - 1) / (16 * MB), s.splits);
-  if (s.splits == 1 || EPI == EPI_PARTIAL) {
-    hipLaunchKernelGGL((gemm_kernel<T, MB, CB, EPI>), grid, dim3(256), 0, st, s, e);
-  } else {
-    GemmEpi pe = e;  // e.part is the partial scratch
-    hipLaunchKernelGGL((gemm_kernel<T, MB, CB, EPI_PARTIAL>), grid, dim3(256), 0, st, s, pe);
-    const int64_t total = (int64_t)s.M * (nbc / 2) * 16;
-    hipLaunchKernelGGL((gemm_finish_kernel<T, EPI>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, s, e,
-                       (const float*)e.part);
+// Sum split-K partials in split order and apply the epilogue (one thread
+// per output element of the launch's column blocks).
+template <typename T>
+__global__ void gemm_finish_kernel(const GemmShape sh, const GemmEpi e, int kind, const float* __restrict__ part) {
+  const int nbc = sh.nb_count ? sh.nb_count : sh.N / 16;
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)sh.M * nbc * 16;
+  if (tid >= total) return;
+  const int c16 = (int)(tid & 15);
+  const int blk = sh.nb_off + (int)((tid >> 4) % nbc);
+  const int row = (int)((tid >> 4) / nbc);
+  float v = 0.f, vp = 0.f;
+  for (int s = 0; s < sh.splits; ++s) {
+    const float* p = part + ((int64_t)s * sh.M + row) * sh.N + 16 * blk;
+    v = (s == 0) ? p[c16] : v + p[c16];
+    vp = (s == 0) ? p[c16 ^ 8] : vp + p[c16 ^ 8];
   }
+  epi_elem<T>(e, kind, sh.N, sh.M, 0, row, blk, c16, v, vp);
+}
+
+template <typename T, int MB, int CBA>
+void gemm_launch(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int nbig, hipStream_t st) {
+  dim3 grid((s.M + 16 * MB - 1) / (16 * MB), nwg, s.splits);
+  hipLaunchKernelGGL((gemm_kernel<T, MB, CBA>), grid, dim3(256), 0, st, s, e, kind, nbig);
 }
 
 template <typename T, int MB>
-void gemm_epi(const GemmShape& s, const GemmEpi& e, hipStream_t st) {
-  switch (e.kind) {
-    case EPI_F32: gemm_go<T, MB, EPI_F32>(s, e, st); break;
-    case EPI_T: gemm_go<T, MB, EPI_T>(s, e, st); break;
-    case EPI_SILU: gemm_go<T, MB, EPI_SILU>(s, e, st); break;
-    case EPI_SWIGLU: gemm_go<T, MB, EPI_SWIGLU>(s, e, st); break;
-    case EPI_QKV: gemm_go<T, MB, EPI_QKV>(s, e, st); break;
-    default: gemm_go<T, MB, EPI_PARTIAL>(s, e, st); break;
+void gemm_mb(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, int nbig, hipStream_t st) {
+  switch (cba) {
+    case 1: gemm_launch<T, MB, 1>(s, e, kind, nwg, nbig, st); break;
+    case 2: gemm_launch<T, MB, 2>(s, e, kind, nwg, nbig, st); break;
+    case 3: gemm_launch<T, MB, 3>(s, e, kind, nwg, nbig, st); break;
+    case 4: gemm_launch<T, MB, 4>(s, e, kind, nwg, nbig, st); break;
+    case 5: gemm_launch<T, MB, 5>(s, e, kind, nwg, nbig, st); break;
+    case 6: gemm_launch<T, MB, 6>(s, e, kind, nwg, nbig, st); break;
+    case 7: gemm_launch<T, MB, 7>(s, e, kind, nwg, nbig, st); break;
+    default: gemm_launch<T, MB, 8>(s, e, kind, nwg, nbig, st); break;
   }
 }
 
 template <typename T>
 void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st) {
+  const int nbc = s.nb_count ? s.nb_count : s.N / 16;
+  // workgroups per slice: GEMM_WGS / splits, at least ceil(nbc / CB_MAX),
+  // at most one per column block; runs of cba or cba - 1 blocks
+  int nwg = (GEMM_WGS + s.splits - 1) / s.splits;
+  nwg = std::max(nwg, (nbc + CB_MAX - 1) / CB_MAX);
+  nwg = std::min(nwg, nbc);
+  const int cba = (nbc + nwg - 1) / nwg;
+  const int nbig = nbc - nwg * (cba - 1);
+  const bool finish = s.splits > 1 && e.kind != EPI_PARTIAL;
+  const int kind = finish ? EPI_PARTIAL : e.kind;
   if (s.M <= 16)
-    gemm_epi<T, 1>(s, e, st);
+    gemm_mb<T, 1>(s, e, kind, nwg, cba, nbig, st);
   else if (s.M <= 32)
-    gemm_epi<T, 2>(s, e, st);
+    gemm_mb<T, 2>(s, e, kind, nwg, cba, nbig, st);
   else
-    gemm_epi<T, 4>(s, e, st);
+    gemm_mb<T, 4>(s, e, kind, nwg, cba, nbig, st);
+  if (finish) {
+    const int64_t total = (int64_t)s.M * nbc * 16;
+    hipLaunchKernelGGL((gemm_finish_kernel<T>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, s, e, e.kind,
+                       (const float*)e.part);
+  }
 }
 
 template <typename T>
@@ -290,7 +333,7 @@ void launch_tile_rows(int dtype, const void* src, int M, int K, void* dst, int m
 }
 
 int gemm_pick_splits(int n_cols, int K, int dtype) {
-  // Wide matrices have enough 64-column groups to fill the GPU on their own;
+  // Wide matrices have enough column blocks to fill the GPU on their own;
   // narrow ones split the reduction so that >= 256 workgroups stream weights.
   const int KB = dtype == DT_BF16 ? 32 : 16;
   const int kblocks = K / KB;
