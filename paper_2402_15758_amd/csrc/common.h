@@ -62,16 +62,52 @@ template <> __device__ __forceinline__ f32x4 mfma_kb<float>(int4 a, int4 b, f32x
 // Butterfly all-reductions over the 64 lanes of a wave.  Each stage adds a
 // lane's value to its partner's in commutative pairs, so every lane ends
 // with bit-identical results.
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = v + __shfl_xor(v, m);
-  return v;
+// Cross-lane combination on the VALU (DPP inside a 16-lane row, gfx950 lane
+// swaps across rows); every lane ends with the same value, combined in a
+// fixed order.  Each step adds a lane's value to its partner's, and the two
+// partners add the same two operands, so they agree bit for bit.
+enum { DPP_XOR1 = 0xB1, DPP_XOR2 = 0x4E, DPP_MIRROR8 = 0x141, DPP_MIRROR16 = 0x140, DPP_ROR8 = 0x128 };
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
-  return v;
+// (even row's value, odd row's value) of each pair of 16-lane rows, and
+// (value in lanes 0-31, value in lanes 32-63), both on every lane
+__device__ __forceinline__ float2 row_pair(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return float2{__uint_as_float(r[0]), __uint_as_float(r[1])};
 }
+__device__ __forceinline__ float2 half_pair(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return float2{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+// over lanes l, l ^ 16, l ^ 32, l ^ 48 (the same position in the four rows)
+__device__ __forceinline__ float rows_sum(float v) {
+  float2 p = row_pair(v);
+  p = half_pair(p.x + p.y);
+  return p.x + p.y;
+}
+__device__ __forceinline__ float rows_max(float v) {
+  float2 p = row_pair(v);
+  p = half_pair(fmaxf(p.x, p.y));
+  return fmaxf(p.x, p.y);
+}
+// over the 16 lanes of a row
+__device__ __forceinline__ float row16_sum(float v) {
+  v = v + dpp_mov<DPP_XOR1>(v);
+  v = v + dpp_mov<DPP_XOR2>(v);
+  v = v + dpp_mov<DPP_MIRROR8>(v);
+  return v + dpp_mov<DPP_MIRROR16>(v);
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_mov<DPP_XOR1>(v));
+  v = fmaxf(v, dpp_mov<DPP_XOR2>(v));
+  v = fmaxf(v, dpp_mov<DPP_MIRROR8>(v));
+  return fmaxf(v, dpp_mov<DPP_MIRROR16>(v));
+}
+// over all 64 lanes (call with every lane active)
+__device__ __forceinline__ float wave_sum(float v) { return rows_sum(row16_sum(v)); }
+__device__ __forceinline__ float wave_max(float v) { return rows_max(row16_max(v)); }
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
 

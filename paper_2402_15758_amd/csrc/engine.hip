@@ -181,6 +181,7 @@ struct chimera_ctx {
   float* part_ml = nullptr;
   int* v_pos = nullptr;
   int64_t* v_kvoff = nullptr;
+  int64_t* rowtab = nullptr;  // [B][TREE_ATTN_TAIL_ROWS]: tail-pass staged rows of the current verify pass
   int* v_qrow = nullptr;
   // draft workspaces
   void* tri_in = nullptr;
@@ -323,6 +324,7 @@ void verify_layers(chimera_ctx* c, const VerifyRows& r, hipStream_t st, bool tim
   const int hdim = H * hd;
   const Gemm g{c, st, timed};
   launch_embed(dt, r.tokens, m->embed, c->x, r.M, d, cf.vocab, st);
+  launch_attn_rows(r.n_b, r.page_table, kv->max_pages, kv->ps, kv->page_stride, hd, r.N, r.B, c->rowtab, st);
   int nparts = 0;
   for (int l = 0; l < cf.n_layers; ++l) {
     const BlockW& w = m->layers[l];
@@ -369,6 +371,7 @@ void verify_layers(chimera_ctx* c, const VerifyRows& r, hipStream_t st, bool tim
     a.out = c->attn;
     a.o_mtiles = c->mt_v;
     a.B = r.B;
+    a.rowtab = c->rowtab;
     launch_tree_attn(dt, a, st);
 
     GemmEpi eo;
@@ -604,6 +607,7 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   const size_t qrows = std::max(B * N, (size_t)64);
   c->part_o = a.arr<float>(qrows * H * c->G * hd);
   c->part_ml = a.arr<float>(qrows * H * c->G * 2);
+  c->rowtab = a.arr<int64_t>(B * TREE_ATTN_TAIL_ROWS);
   c->v_pos = a.arr<int>(Mv);
   c->v_kvoff = a.arr<int64_t>(Mv);
   c->v_qrow = a.arr<int>(Mv);

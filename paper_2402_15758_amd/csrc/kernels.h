@@ -96,8 +96,16 @@ struct TreeAttnArgs {
   void* out;                // tiled [B*N][H*hd] with o_mtiles tiles
   int o_mtiles;
   int B;
+  const int64_t* rowtab;    // [B][TREE_ATTN_TAIL_ROWS] from launch_attn_rows
 };
 void launch_tree_attn(int dtype, const TreeAttnArgs& a, hipStream_t st);
+// Rows the tail pass stages per sequence: the committed positions of the last
+// chunks (<= 127) and the N tree slots, i.e. positions lo .. n + N - 1.
+constexpr int TREE_ATTN_TAIL_ROWS = 192;
+// rowtab[b][rr] = page-resolved element offset (head and layer excluded) of
+// position lo_b + rr, written once per verify pass for all layers.
+void launch_attn_rows(const int* n_b, const int* page_table, int max_pages, int ps, int64_t page_stride, int hd,
+                      int N, int B, int64_t* rowtab, hipStream_t st);
 
 struct EncAttnArgs {
   const void* q;            // [B][ldq]

@@ -10,7 +10,8 @@
 //     shared by every query of the tree: an MFMA pass over groups of two
 //     chunks writes one partial (m, l, O) per group;
 //   * the last two chunks c_u - 1 and c_u, which contain every tree
-//     position, are reduced per query by a VALU pass that first folds the
+//     position, are reduced per query (scores by MFMA over the staged rows,
+//     softmax and PV on the VALU in logical key order) after folding the
 //     group partials in group order.
 // The decomposition depends on P_u alone, so a query gets bit-identical
 // results whether it is a node of a 64-node tree or the single query of a
@@ -24,6 +25,27 @@ constexpr int CHUNK = 64;   // positions per chunk
 constexpr int GROUP = TREE_ATTN_GROUP_POSITIONS / CHUNK;  // chunks per shared-pass workgroup
 constexpr int TAIL_ROWS = 2 * CHUNK;  // committed rows staged by the tail pass
 constexpr int MAX_NODES = 64;
+constexpr int TAIL_QPW = 8;  // queries (one wave each) per tail-pass workgroup
+static_assert(TAIL_ROWS + MAX_NODES == TREE_ATTN_TAIL_ROWS, "tail rows");
+
+// Page-resolved offsets of the tail pass's staged rows (positions lo .. n+N-1
+// with lo = 64 * max(n / 64 - 1, 0)); entries past them are zero.
+__global__ void attn_rows_kernel(const int* __restrict__ n_b, const int* __restrict__ page_table, int max_pages,
+                                 int ps, int64_t page_stride, int hd, int N, int64_t* __restrict__ rowtab) {
+  const int b = blockIdx.x;
+  const int n = n_b[b];
+  const int cmin = n / CHUNK;
+  const int lo = (cmin >= 1 ? cmin - 1 : 0) * CHUNK;
+  const int nrows = n - lo + N;
+  for (int rr = threadIdx.x; rr < TREE_ATTN_TAIL_ROWS; rr += blockDim.x) {
+    int64_t off = 0;
+    if (rr < nrows) {
+      const int p = lo + rr;
+      off = (int64_t)page_table[(int64_t)b * max_pages + p / ps] * page_stride + (int64_t)(p % ps) * hd;
+    }
+    rowtab[(int64_t)b * TREE_ATTN_TAIL_ROWS + rr] = off;
+  }
+}
 
 // ---------------------------------------------------------------------------
 // Shared pass: grid (group slots, H, B), 4 waves; wave w owns queries
@@ -55,16 +77,26 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   }
   const int dep_u = a.depth[uu];
   const int n = a.n_b[b];
+  // the group's page ids need no n: load them with it
+  const int c_begin = grp * GROUP;
+  constexpr int PB = (GROUP * CHUNK + 255) / 256;
+  int pg[PB];
+#pragma unroll
+  for (int t = 0; t < PB; ++t) {
+    const int i = tid + 256 * t;
+    const int pi = (c_begin * CHUNK + i) / a.ps;
+    pg[t] = (i < GROUP * CHUNK && pi < a.max_pages) ? a.page_table[(int64_t)b * a.max_pages + pi] : 0;
+  }
   const int cmax = (n + a.D) / CHUNK;
   const int last = cmax - 2;            // last chunk any query treats as shared
-  const int c_begin = grp * GROUP;
   if (c_begin > last) return;
   const int c_end = min(c_begin + GROUP - 1, last);
   const int lim_u = (n + dep_u) / CHUNK - 2;
-  for (int i = tid; i < (c_end - c_begin + 1) * CHUNK; i += 256) {
+#pragma unroll
+  for (int t = 0; t < PB; ++t) {
+    const int i = tid + 256 * t;
     const int p = c_begin * CHUNK + i;
-    pbase[i] = (int64_t)a.page_table[(int64_t)b * a.max_pages + p / a.ps] * a.page_stride +
-               ((int64_t)h * a.ps + p % a.ps) * HD;
+    if (i < GROUP * CHUNK) pbase[i] = (int64_t)pg[t] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD;
   }
   __syncthreads();
   float m = -CH_INF, l = 0.f;
@@ -122,8 +154,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
         s[kb][r] = v;
         mc = fmaxf(mc, v);
       }
-    mc = fmaxf(mc, __shfl_xor(mc, 16));
-    mc = fmaxf(mc, __shfl_xor(mc, 32));
+    mc = rows_max(mc);
     const float mn = fmaxf(m, mc);
     float alpha = 1.f, ls = 0.f;
     if (mn != -CH_INF) {
@@ -140,8 +171,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    ls = ls + __shfl_xor(ls, 16);
-    ls = ls + __shfl_xor(ls, 32);
+    ls = rows_sum(ls);
     l = l * alpha + ls;
     m = mn;
 #pragma unroll
@@ -190,59 +220,60 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tail pass: grid (ceil(N/16), H, B), 16 waves; wave w reduces query
-// 16*blockIdx.x + w.  The committed rows of the last chunks and every tree
-// slot are staged in LDS once per workgroup.  Loads that do not depend on
-// each other are issued together: (query, n) -> (page offsets, tree paths,
-// first batch of shared-pass partials) -> staged rows.
+// Tail pass: grid (ceil(N/QPW), H, B), QPW = TAIL_QPW waves (one workgroup
+// per CU at the 64-node tree and 32 heads); wave w reduces query
+// u = QPW * blockIdx.x + w.  The workgroup stages the committed positions
+// lo .. n-1 of the last chunks followed by every tree slot (rows 0 .. nrows-1):
+//   1. loads that need nothing: n, the staged rows' page-resolved offsets
+//      (written once per pass), the queries' MFMA fragments, tree paths and
+//      depths, the first batch of shared-pass partials;
+//   2. K fragments and V rows are requested; while they are in flight each
+//      wave folds its query's partials in group order; then S = Q K^T over
+//      every staged row by MFMA -> LDS, and V -> LDS as float;
+//   3. per query: the last two chunks in logical-position order (lane = key);
+//      PV on the VALU.
+// Each score is one MFMA dot product whose value does not depend on where
+// the query or key sits in the tile, so a query's scores are the same in a
+// tree and in a single-query step.
 // ---------------------------------------------------------------------------
 template <typename T, int HD>
-__global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
+__global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnArgs a) {
+  constexpr int NT = 64 * TAIL_QPW;
   constexpr int VEC = ET<T>::VEC;
-  constexpr int KP = HD + VEC;
-  constexpr int ROWS = TAIL_ROWS + MAX_NODES;
-  constexpr int DPL = HD / 64;  // output dims per lane
+  constexpr int KB = 4 * VEC;                 // reduction indices per MFMA k-block
+  constexpr int ROWS = TAIL_ROWS + MAX_NODES;  // staged rows, upper bound
+  constexpr int DPL = HD / 64;                 // output dims per lane
   constexpr int PARTS = HD / VEC;
-  constexpr int BATCH = 8;      // shared-pass partials loaded per round trip
+  constexpr int BATCH = 8;                     // shared-pass partials loaded per round trip
+  constexpr int PV_BATCH = 16;                 // keys whose V rows are read per round
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  T* Kl = reinterpret_cast<T*>(smem);
-  T* Vl = Kl + ROWS * KP;
-  float* qs = reinterpret_cast<float*>(Vl + ROWS * HD);
+  float* Vl = reinterpret_cast<float*>(smem);  // [ROWS][HD]
+  float* Sl = Vl + ROWS * HD;                  // [QPW][ROWS]
   __shared__ int64_t rowbase[ROWS];
-  __shared__ uint8_t spath[16][64];
-  __shared__ int sdepth[16];
+  __shared__ uint8_t spath[TAIL_QPW][64];
+  __shared__ int sdepth[TAIL_QPW];
 
   const int h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int u = 16 * blockIdx.x + wave;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  const int u0 = TAIL_QPW * blockIdx.x;
+  const int u = u0 + wave;
   const bool active = u < a.N;
-  // round trip 1: the query row, n, tree metadata of this workgroup's queries
-  T qv[DPL];
-  if (active) {
-    const T* qrow = (const T*)a.q + (int64_t)(b * a.N + u) * a.ldq + h * HD + DPL * lane;
+  // 1. loads that need nothing
+  const int n = a.n_b[b];
+  int4 qf[HD / KB];  // MFMA A operand: row c16 = query u0 + c16 (zero beyond the workgroup's queries)
+  {
+    const int uq = u0 + c16;
+    const bool qok = c16 < TAIL_QPW && uq < a.N;
+    const T* qrow = (const T*)a.q + (int64_t)(b * a.N + (qok ? uq : 0)) * a.ldq + h * HD + g * VEC;
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) qv[e] = qrow[e];
+    for (int ks = 0; ks < HD / KB; ++ks) qf[ks] = qok ? ld16(qrow + ks * KB) : int4{0, 0, 0, 0};
   }
-  for (int i = tid; i < 16 * 64; i += 1024) {
-    const int uu = 16 * blockIdx.x + i / 64;
+  for (int i = tid; i < TAIL_QPW * 64; i += NT) {
+    const int uu = u0 + i / 64;
     spath[i / 64][i % 64] = uu < a.N ? a.path[uu * 64 + i % 64] : 0;
   }
-  if (tid < 16) sdepth[tid] = (16 * blockIdx.x + tid) < a.N ? a.depth[16 * blockIdx.x + tid] : 0;
-  const int n = a.n_b[b];
-  const int cmin = n / CHUNK;
-  const int lo = (cmin >= 1 ? cmin - 1 : 0) * CHUNK;  // first staged committed position
-  const int nc = n - lo;                               // committed rows staged (<= 127)
-  const T* kpool = (const T*)a.kpool;
-  const T* vpool = (const T*)a.vpool;
-  const int* ptab = a.page_table + (int64_t)b * a.max_pages;
-  const int nrows_total = nc + a.N;
-  // round trip 2: page offsets of the staged rows, first batch of partials
-  for (int rr = tid; rr < nrows_total; rr += 1024) {
-    const int p = rr < nc ? lo + rr : n + (rr - nc);
-    rowbase[rr] = (int64_t)ptab[p / a.ps] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD;
-  }
-  // groups every query of the tree folds are bounded by those of the deepest node
-  const int ngrp_max = ((n + a.D) / CHUNK - 2) >= 0 ? ((n + a.D) / CHUNK - 2) / GROUP + 1 : 0;
+  if (tid < TAIL_QPW) sdepth[tid] = (u0 + tid) < a.N ? a.depth[u0 + tid] : 0;
   float bm[BATCH], bl[BATCH], bo[BATCH][DPL];
   auto load_batch = [&](int g0) {
 #pragma unroll
@@ -251,7 +282,7 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
       bl[t] = 0.f;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) bo[t][e] = 0.f;
-      if (active && g0 + t < ngrp_max) {
+      if (active && g0 + t < a.G) {  // slots past this step's groups are read but never folded
         const int64_t slot = (((int64_t)b * a.H + h) * a.G + g0 + t) * a.N + u;
         bm[t] = a.part_ml[slot * 2];
         bl[t] = a.part_ml[slot * 2 + 1];
@@ -261,49 +292,45 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
     }
   };
   load_batch(0);
-  if (active) {
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) qs[wave * HD + DPL * lane + e] = ET<T>::to_f(qv[e]);
-  }
+  const int64_t hoff = (int64_t)h * a.ps * HD;
+  for (int rr = tid; rr < ROWS; rr += NT) rowbase[rr] = a.rowtab[(int64_t)b * ROWS + rr] + hoff;
+  const int cmin = n / CHUNK;
+  const int lo = (cmin >= 1 ? cmin - 1 : 0) * CHUNK;  // first staged committed position
+  const int nc = n - lo;                               // committed rows staged (<= 127)
+  const int nrows = nc + a.N;
   __syncthreads();
-  // round trip 3: the staged rows
-  {
-    constexpr int UNR = (ROWS * PARTS + 1023) / 1024;
-    int4 kbuf[UNR], vbuf[UNR];
+  // 2. V rows -> LDS (float); scores by MFMA -> LDS
+  const T* kpool = (const T*)a.kpool;
+  const T* vpool = (const T*)a.vpool;
+  // every load of this phase is issued before any is used: K fragments of
+  // the wave's row tiles (wave w takes tiles w and w + QPW), then V rows
+  constexpr int RT_PER_WAVE = (ROWS / 16 + TAIL_QPW - 1) / TAIL_QPW;
+  int4 kf[RT_PER_WAVE][HD / KB];
 #pragma unroll
-    for (int t = 0; t < UNR; ++t) {
-      const int idx = tid + 1024 * t;
-      if (idx < nrows_total * PARTS) {
-        const int64_t base = rowbase[idx / PARTS] + (idx % PARTS) * VEC;
-        kbuf[t] = ld16(kpool + base);
-        vbuf[t] = ld16(vpool + base);
-      }
-    }
+  for (int j = 0; j < RT_PER_WAVE; ++j) {
+    const int rr = 16 * (wave + TAIL_QPW * j) + c16;  // MFMA B column: staged row
+    const T* kr = kpool + rowbase[rr < nrows ? rr : 0] + g * VEC;
 #pragma unroll
-    for (int t = 0; t < UNR; ++t) {
-      const int idx = tid + 1024 * t;
-      if (idx < nrows_total * PARTS) {
-        const int rr = idx / PARTS, part = idx % PARTS;
-        const int dst = rr < nc ? rr : TAIL_ROWS + (rr - nc);
-        st16(&Kl[dst * KP + part * VEC], kbuf[t]);
-        st16(&Vl[dst * HD + part * VEC], vbuf[t]);
-      }
-    }
+    for (int ks = 0; ks < HD / KB; ++ks) kf[j][ks] = ld16(kr + ks * KB);
   }
-  __syncthreads();
-  if (!active) return;
-
-  const float* q = qs + wave * HD;
+  constexpr int UNR = (ROWS * PARTS + NT - 1) / NT;
+  int4 vbuf[UNR];
+#pragma unroll
+  for (int t = 0; t < UNR; ++t) {  // unpredicated: slots past the staged rows re-read row 0
+    const int idx = tid + NT * t;
+    const int rr = idx < nrows * PARTS ? idx / PARTS : 0;
+    vbuf[t] = ld16(vpool + rowbase[rr] + (idx % PARTS) * VEC);
+  }
+  // while those loads are in flight: fold the shared-pass partials of this
+  // wave's query in group order
   const int Pu = n + sdepth[wave];
   const int cu = Pu / CHUNK;
-  // fold the shared-pass partials in group order
   float m = -CH_INF, l = 0.f, o[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) o[e] = 0.f;
   const int lim = cu - 2;
-  const int ngrp = lim >= 0 ? lim / GROUP + 1 : 0;
-  for (int g0 = 0; g0 < ngrp; g0 += BATCH) {
-    if (g0 > 0) load_batch(g0);
+  const int ngrp = (active && lim >= 0) ? lim / GROUP + 1 : 0;
+  auto fold_batch = [&](int g0) {
 #pragma unroll
     for (int t = 0; t < BATCH; ++t) {
       if (g0 + t >= ngrp || bm[t] == -CH_INF) continue;
@@ -314,7 +341,45 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
       for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + bo[t][e] * a2;
       m = mn;
     }
+  };
+  // the first batch was loaded before the K/V requests: straight-line code
+  // here lets its wait leave those in flight
+  fold_batch(0);
+  for (int g0 = BATCH; g0 < ngrp; g0 += BATCH) {
+    load_batch(g0);
+    fold_batch(g0);
   }
+#pragma unroll
+  for (int j = 0; j < RT_PER_WAVE; ++j) {
+    const int rt = wave + TAIL_QPW * j;
+    if (16 * rt >= nrows) break;  // wave-uniform
+    const int rr = 16 * rt + c16;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < HD / KB; ++ks) acc = mfma_kb<T>(qf[ks], kf[j][ks], acc);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int qi = 4 * g + r;  // output row = query
+      if (qi < TAIL_QPW && rr < nrows) Sl[qi * ROWS + rr] = acc[r];
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < UNR; ++t) {
+    const int idx = tid + NT * t;
+    if (idx < nrows * PARTS) {
+      const T* ve = reinterpret_cast<const T*>(&vbuf[t]);
+      float* dst = &Vl[(idx / PARTS) * HD + (idx % PARTS) * VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; e += 4)
+        *reinterpret_cast<float4*>(dst + e) =
+            float4{ET<T>::to_f(ve[e]), ET<T>::to_f(ve[e + 1]), ET<T>::to_f(ve[e + 2]), ET<T>::to_f(ve[e + 3])};
+    }
+  }
+  __syncthreads();
+  if (!active) return;
+
+  // 3. per query: the last two chunks, keys in logical-position order
+  const float* srow = Sl + wave * ROWS;
   // the last two chunks, keys in logical-position order
   for (int c = (cu >= 1 ? cu - 1 : 0); c <= cu; ++c) {
     const int p = c * CHUNK + lane;
@@ -322,24 +387,12 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
     int row = 0;
     float s = -CH_INF;
     if (valid) {
-      row = p < n ? p - lo : TAIL_ROWS + (int)spath[wave][p - n];
-      const T* kr = &Kl[row * KP];
-      float acc = 0.f;
-#pragma unroll
-      for (int part = 0; part < PARTS; ++part) {
-        const int4 kv = ld16(kr + part * VEC);
-        const T* ke = reinterpret_cast<const T*>(&kv);
-#pragma unroll
-        for (int e4 = 0; e4 < VEC; e4 += 4) {
-          const float4 qq = *reinterpret_cast<const float4*>(q + part * VEC + e4);
-          acc = fmaf(qq.x, ET<T>::to_f(ke[e4 + 0]), acc);
-          acc = fmaf(qq.y, ET<T>::to_f(ke[e4 + 1]), acc);
-          acc = fmaf(qq.z, ET<T>::to_f(ke[e4 + 2]), acc);
-          acc = fmaf(qq.w, ET<T>::to_f(ke[e4 + 3]), acc);
-        }
-      }
-      s = acc * a.scale;
+      row = p < n ? p - lo : nc + (int)spath[wave][p - n];
+      s = srow[row] * a.scale;
     }
+    // lane 0 holds the chunk's first key, always one of the query's keys
+    const int row0 = __builtin_amdgcn_readlane(row, 0);
+    if (!valid) row = row0;
     const float mc = wave_max(s);
     const float mn = fmaxf(m, mc);
     const float alpha = exp_diff(m, mn);
@@ -347,22 +400,25 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
     l = l * alpha + wave_sum(pe);
 #pragma unroll
     for (int e = 0; e < DPL; ++e) o[e] = o[e] * alpha;
-    const int cnt = min(CHUNK, Pu - c * CHUNK + 1);
+    // keys in order, 16 per round: the 16 V rows are read before any is used.
+    // Keys past the query's last one in a round have pe = 0 and the staged
+    // row of the chunk's first key, so they add exact zeros.
+    const int cnt = __builtin_amdgcn_readfirstlane(min(CHUNK, Pu - c * CHUNK + 1));
+    for (int i0 = 0; i0 < cnt; i0 += PV_BATCH) {
+      float pis[PV_BATCH];
+      float vv[PV_BATCH][DPL];
 #pragma unroll
-    for (int i = 0; i < CHUNK; ++i) {
-      if (i < cnt) {
-        const float pi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pe), i));
-        const int ri = __builtin_amdgcn_readlane(row, i);
-        const T* vr = &Vl[ri * HD + DPL * lane];
-        if constexpr (sizeof(T) == 2 && DPL == 2) {
-          const uint32_t u2 = *reinterpret_cast<const uint32_t*>(vr);
-          o[0] = fmaf(pi, __uint_as_float(u2 << 16), o[0]);
-          o[1] = fmaf(pi, __uint_as_float(u2 & 0xffff0000u), o[1]);
-        } else {
+      for (int j = 0; j < PV_BATCH; ++j) {
+        pis[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pe), i0 + j));
+        const int ri = __builtin_amdgcn_readlane(row, i0 + j);
+        const float* vr = &Vl[ri * HD + DPL * lane];
 #pragma unroll
-          for (int e = 0; e < DPL; ++e) o[e] = fmaf(pi, ET<T>::to_f(vr[e]), o[e]);
-        }
+        for (int e = 0; e < DPL; ++e) vv[j][e] = vr[e];
       }
+#pragma unroll
+      for (int j = 0; j < PV_BATCH; ++j)
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) o[e] = fmaf(pis[j], vv[j][e], o[e]);
     }
     m = mn;
   }
@@ -373,15 +429,15 @@ __global__ __launch_bounds__(1024) void tree_attn_tail(const TreeAttnArgs a) {
 template <typename T, int HD>
 void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((tree_attn_shared<T, HD>), dim3(a.G, a.H, a.B), dim3(256), 0, st, a);
-  constexpr int VEC = ET<T>::VEC;
-  const size_t smem = (size_t)(TAIL_ROWS + MAX_NODES) * ((HD + VEC) + HD) * sizeof(T) + 16 * HD * sizeof(float);
+  const size_t smem = (size_t)(TAIL_ROWS + MAX_NODES) * (HD + TAIL_QPW) * sizeof(float);
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)tree_attn_tail<T, HD>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)smem);
     attr_set = true;
   }
-  hipLaunchKernelGGL((tree_attn_tail<T, HD>), dim3((a.N + 15) / 16, a.H, a.B), dim3(1024), smem, st, a);
+  hipLaunchKernelGGL((tree_attn_tail<T, HD>), dim3((a.N + TAIL_QPW - 1) / TAIL_QPW, a.H, a.B), dim3(64 * TAIL_QPW),
+                     smem, st, a);
 }
 
 // ---------------------------------------------------------------------------
@@ -428,15 +484,11 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
 #pragma unroll
       for (int e = 0; e < DS; ++e) d = fmaf(q[e], ET<T>::to_f(kr[e]), d);
     }
-    d = d + __shfl_xor(d, 1);
-    d = d + __shfl_xor(d, 2);
-    d = d + __shfl_xor(d, 4);
-    d = d + __shfl_xor(d, 8);
+    d = row16_sum(d);
     sc[kg] = key < nkeys ? d * a.scale : -CH_INF;
     mloc = fmaxf(mloc, sc[kg]);
   }
-  mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-  const float mw = fmaxf(mloc, __shfl_xor(mloc, 32));
+  const float mw = rows_max(mloc);
   float lsum = 0.f, o[DS];
 #pragma unroll
   for (int e = 0; e < DS; ++e) o[e] = 0.f;
@@ -451,12 +503,10 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
       for (int e = 0; e < DS; ++e) o[e] = fmaf(p, ET<T>::to_f(vr[e]), o[e]);
     }
   }
-  lsum = lsum + __shfl_xor(lsum, 16);
-  lsum = lsum + __shfl_xor(lsum, 32);
+  lsum = rows_sum(lsum);
 #pragma unroll
   for (int e = 0; e < DS; ++e) {
-    o[e] = o[e] + __shfl_xor(o[e], 16);
-    o[e] = o[e] + __shfl_xor(o[e], 32);
+    o[e] = rows_sum(o[e]);
   }
   if (lane == 0) {
     wm[wave] = mw;
@@ -516,6 +566,12 @@ void enc_attn_go(const EncAttnArgs& a, hipStream_t st) {
 }
 
 }  // namespace
+
+void launch_attn_rows(const int* n_b, const int* page_table, int max_pages, int ps, int64_t page_stride, int hd,
+                      int N, int B, int64_t* rowtab, hipStream_t st) {
+  hipLaunchKernelGGL(attn_rows_kernel, dim3(B), dim3(TREE_ATTN_TAIL_ROWS), 0, st, n_b, page_table, max_pages, ps,
+                     page_stride, hd, N, rowtab);
+}
 
 void launch_tree_attn(int dtype, const TreeAttnArgs& a, hipStream_t st) {
   if (dtype == DT_BF16 && a.hd == 128)

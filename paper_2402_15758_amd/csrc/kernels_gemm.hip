@@ -218,7 +218,7 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
     for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * CB + j) * 64 + lane];
     f32x4 vp;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) vp[r] = __shfl_xor(v[r], 8);
+    for (int r = 0; r < 4; ++r) vp[r] = dpp_mov<DPP_ROR8>(v[r]);  // lane column c16 ^ 8
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = 16 * (mb0 + i) + 4 * g + r;
