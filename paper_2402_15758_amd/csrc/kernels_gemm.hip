@@ -127,6 +127,38 @@ __device__ __forceinline__ void epi_elem(const GemmEpi& e, int kind, int N, int 
   }
 }
 
+// Per-row targets of the QKV epilogue, staged in LDS before the k-loop.
+struct RowMeta {
+  int64_t kvoff;  // K/V element offset (-1: skip)
+  int pos;        // rotary position
+  int qrow;       // Q output row (-1: skip)
+};
+
+// QKV epilogue of one element with its rotary cos/sin already loaded (the
+// same arithmetic as epi_elem's EPI_QKV branch).
+template <typename T>
+__device__ __forceinline__ void qkv_store(const GemmEpi& e, const RowMeta& rm, int blk, int c16, float v, float vp,
+                                          float c, float s) {
+  const int hd = e.hd;
+  const int blk_head = hd / 16;
+  const int sec_blks = e.H * blk_head;
+  const int sec = blk / sec_blks, rem = blk % sec_blks;
+  const int h = rem / blk_head, q = rem % blk_head;
+  if (sec < 2) {
+    const bool first = c16 < 8;
+    const int i = 8 * q + (c16 & 7);
+    const float o = first ? v * c - vp * s : v * c + vp * s;
+    const int dim = first ? i : i + hd / 2;
+    if (sec == 0) {
+      if (rm.qrow >= 0) ((T*)e.qout)[(int64_t)rm.qrow * e.ldq + h * hd + dim] = ET<T>::from_f(o);
+    } else if (rm.kvoff >= 0) {
+      ((T*)e.kbase)[rm.kvoff + h * e.head_stride + dim] = ET<T>::from_f(o);
+    }
+  } else if (rm.kvoff >= 0) {
+    ((T*)e.vbase)[rm.kvoff + h * e.head_stride + 16 * q + c16] = ET<T>::from_f(v);
+  }
+}
+
 template <typename T>
 __device__ __forceinline__ int4 ldw(const T* p) {
   typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -139,7 +171,7 @@ __device__ __forceinline__ int4 ldw(const T* p) {
 // [4][MB][CB][64] f32x4.
 template <typename T, int MB, int CB, int PF>
 __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0, int kbeg,
-                                         int kend, f32x4* red) {
+                                         int kend, f32x4* red, const RowMeta* rm) {
   constexpr int VEC = ET<T>::VEC;
   // The wave index is made provably wave-uniform so that every branch of the
   // k-loop below is a scalar branch: an MFMA ignores EXEC, so it must never
@@ -211,18 +243,66 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
 #pragma unroll
     for (int j = 0; j < CB; ++j) red[((wave * MB + i) * CB + j) * 64 + lane] = acc[i][j];
   __syncthreads();
-  for (int it = wave; it < MB * CB; it += 4) {
+  // this wave's output tiles: items it = wave, wave + 4, ... of MB * CB
+  constexpr int ITEMS = (MB * CB + 3) / 4;
+  f32x4 vv[ITEMS], vpp[ITEMS];
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const int it = wave + 4 * k;
+    if (it < MB * CB) {  // wave-uniform
+      const int i = it / CB, j = it % CB;
+      f32x4 v = red[((0 * MB + i) * CB + j) * 64 + lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * CB + j) * 64 + lane];
+      vv[k] = v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vpp[k][r] = dpp_mov<DPP_ROR8>(v[r]);  // lane column c16 ^ 8
+    }
+  }
+  if (kind == EPI_QKV) {
+    // rotary tables for every element first, then the stores
+    float cs[ITEMS][4], sn[ITEMS][4];
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+      const int it = wave + 4 * k;
+      const int i = it / CB, j = it % CB;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        cs[k][r] = 1.f;
+        sn[k][r] = 0.f;
+        const int lr = 16 * i + 4 * g + r;
+        const int row = 16 * mb0 + lr;
+        const int q = (cb0 + j) % (e.hd / 16);
+        const bool rot = (cb0 + j) < 2 * e.H * (e.hd / 16);
+        if (it < MB * CB && row < sh.M && rot) {
+          const int64_t ti = (int64_t)rm[lr].pos * (e.hd / 2) + 8 * q + (c16 & 7);
+          cs[k][r] = e.rcos[ti];
+          sn[k][r] = e.rsin[ti];
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+      const int it = wave + 4 * k;
+      const int i = it / CB, j = it % CB;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lr = 16 * i + 4 * g + r;
+        const int row = 16 * mb0 + lr;
+        if (it < MB * CB && row < sh.M) qkv_store<T>(e, rm[lr], cb0 + j, c16, vv[k][r], vpp[k][r], cs[k][r], sn[k][r]);
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const int it = wave + 4 * k;
     const int i = it / CB, j = it % CB;
-    f32x4 v = red[((0 * MB + i) * CB + j) * 64 + lane];
-#pragma unroll
-    for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * CB + j) * 64 + lane];
-    f32x4 vp;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) vp[r] = dpp_mov<DPP_ROR8>(v[r]);  // lane column c16 ^ 8
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = 16 * (mb0 + i) + 4 * g + r;
-      if (row < sh.M) epi_elem<T>(e, kind, sh.N, sh.M, blockIdx.z, row, cb0 + j, c16, v[r], vp[r]);
+      if (it < MB * CB && row < sh.M)
+        epi_elem<T>(e, kind, sh.N, sh.M, blockIdx.z, row, cb0 + j, c16, vv[k][r], vpp[k][r]);
     }
   }
 }
@@ -239,12 +319,21 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const Gem
   const int kend = kbeg + kps;
   const int b = blockIdx.y;
   const int mb0 = blockIdx.x * MB;
+  // QKV epilogue targets of this workgroup's rows (visible after the k-loop's
+  // barrier)
+  __shared__ RowMeta rm[16 * MB];
+  if (kind == EPI_QKV && threadIdx.x < 16 * MB) {
+    const int row = 16 * mb0 + threadIdx.x;
+    RowMeta t{-1, 0, -1};
+    if (row < sh.M) t = RowMeta{e.kvoff[row], e.pos[row], e.qrow[row]};
+    rm[threadIdx.x] = t;
+  }
   if (b < nbig) {
-    gemm_run<T, MB, CBA, PF>(sh, e, kind, sh.nb_off + b * CBA, mb0, kbeg, kend, red);
+    gemm_run<T, MB, CBA, PF>(sh, e, kind, sh.nb_off + b * CBA, mb0, kbeg, kend, red, rm);
   } else {
     if constexpr (CBA > 1)
       gemm_run<T, MB, CBA - 1, PF>(sh, e, kind, sh.nb_off + nbig * CBA + (b - nbig) * (CBA - 1), mb0, kbeg, kend,
-                                   red);
+                                   red, rm);
   }
 }
 
