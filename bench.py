@@ -189,9 +189,9 @@ def main():
             out[b] += [int(x) for x in toks[b, : n[b]]]
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    # profiled pass: K more steps with HIP events around each phase and each
-    # verify GEMM launch, on the stream the kernels run on (kernels launched
-    # one by one here, so each event pair brackets one kernel)
+    # profiled pass: K more steps with HIP events on the stream the kernels
+    # run on: around each phase, and recorded by each verify GEMM kernel's
+    # own dispatch at its start and end (kernels launched one by one here)
     spec.set_graph(False)
     spec.profile(True)
     accepted_p = 0

@@ -297,10 +297,17 @@ struct Gemm {
       const double es = (double)c->m->es;
       c->ev_bytes[c->ev_used] = (double)K * cols * es + (double)M * K * es + (double)M * cols * 4.0;
       c->ev_used++;
-      HIPCK(hipEventRecord(ev->a, st));
     }
-    launch_gemm(c->m->dt, s, e, st);
-    if (ev) HIPCK(hipEventRecord(ev->b, st));
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (ev) HIPCK(hipStreamIsCapturing(st, &cap));
+    if (ev && cap == hipStreamCaptureStatusNone) {
+      // launched kernels record the events at their own start and end
+      launch_gemm(c->m->dt, s, e, st, ev->a, ev->b);
+    } else {
+      if (ev) HIPCK(hipEventRecord(ev->a, st));
+      launch_gemm(c->m->dt, s, e, st);
+      if (ev) HIPCK(hipEventRecord(ev->b, st));
+    }
   }
   int splits(int N, int K) const { return gemm_pick_splits(N, K, c->m->dt); }
 };

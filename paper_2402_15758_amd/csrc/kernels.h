@@ -57,7 +57,10 @@ struct GemmShape {
 
 // Splits chosen from (N, K) only, never from M.
 int gemm_pick_splits(int n_cols, int K, int dtype);
-void launch_gemm(int dtype, const GemmShape& s, const GemmEpi& e, hipStream_t st);
+// ev_start / ev_stop (optional): recorded by the dispatch of the GEMM's
+// first and last kernel (hipExtLaunchKernel), i.e. the kernel execution span.
+void launch_gemm(int dtype, const GemmShape& s, const GemmEpi& e, hipStream_t st, hipEvent_t ev_start = nullptr,
+                 hipEvent_t ev_stop = nullptr);
 void launch_repack(int dtype, int kind, const void* src0, const void* src1, const void* src2, int K, int n_src,
                    void* dst, int H, int hd, hipStream_t st);
 // Row-major [M][K] -> tiled (test hook and one-off conversions).

@@ -20,6 +20,8 @@
 // slice order by their consumer (the next norm) or by a finishing pass that
 // applies the epilogue.  Every row's arithmetic depends only on (N, K): the
 // same row gives identical bits whether a launch carries 1 or 256 rows.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 
 #include "common.h"
@@ -358,27 +360,32 @@ __global__ void gemm_finish_kernel(const GemmShape sh, const GemmEpi e, int kind
 }
 
 template <typename T, int MB, int CBA>
-void gemm_launch(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int nbig, hipStream_t st) {
+void gemm_launch(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int nbig, hipStream_t st, hipEvent_t ea,
+                 hipEvent_t eb) {
   dim3 grid((s.M + 16 * MB - 1) / (16 * MB), nwg, s.splits);
-  hipLaunchKernelGGL((gemm_kernel<T, MB, CBA>), grid, dim3(256), 0, st, s, e, kind, nbig);
+  if (ea || eb)
+    hipExtLaunchKernelGGL((gemm_kernel<T, MB, CBA>), grid, dim3(256), 0, st, ea, eb, 0, s, e, kind, nbig);
+  else
+    hipLaunchKernelGGL((gemm_kernel<T, MB, CBA>), grid, dim3(256), 0, st, s, e, kind, nbig);
 }
 
 template <typename T, int MB>
-void gemm_mb(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, int nbig, hipStream_t st) {
+void gemm_mb(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, int nbig, hipStream_t st,
+             hipEvent_t ea, hipEvent_t eb) {
   switch (cba) {
-    case 1: gemm_launch<T, MB, 1>(s, e, kind, nwg, nbig, st); break;
-    case 2: gemm_launch<T, MB, 2>(s, e, kind, nwg, nbig, st); break;
-    case 3: gemm_launch<T, MB, 3>(s, e, kind, nwg, nbig, st); break;
-    case 4: gemm_launch<T, MB, 4>(s, e, kind, nwg, nbig, st); break;
-    case 5: gemm_launch<T, MB, 5>(s, e, kind, nwg, nbig, st); break;
-    case 6: gemm_launch<T, MB, 6>(s, e, kind, nwg, nbig, st); break;
-    case 7: gemm_launch<T, MB, 7>(s, e, kind, nwg, nbig, st); break;
-    default: gemm_launch<T, MB, 8>(s, e, kind, nwg, nbig, st); break;
+    case 1: gemm_launch<T, MB, 1>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 2: gemm_launch<T, MB, 2>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 3: gemm_launch<T, MB, 3>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 4: gemm_launch<T, MB, 4>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 5: gemm_launch<T, MB, 5>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 6: gemm_launch<T, MB, 6>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 7: gemm_launch<T, MB, 7>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    default: gemm_launch<T, MB, 8>(s, e, kind, nwg, nbig, st, ea, eb); break;
   }
 }
 
 template <typename T>
-void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st) {
+void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int nbc = s.nb_count ? s.nb_count : s.N / 16;
   // workgroups per slice: GEMM_WGS / splits, at least ceil(nbc / CB_MAX),
   // at most one per column block; runs of cba or cba - 1 blocks
@@ -389,16 +396,21 @@ void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st) {
   const int nbig = nbc - nwg * (cba - 1);
   const bool finish = s.splits > 1 && e.kind != EPI_PARTIAL;
   const int kind = finish ? EPI_PARTIAL : e.kind;
+  hipEvent_t eb = finish ? nullptr : ev_stop;
   if (s.M <= 16)
-    gemm_mb<T, 1>(s, e, kind, nwg, cba, nbig, st);
+    gemm_mb<T, 1>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   else if (s.M <= 32)
-    gemm_mb<T, 2>(s, e, kind, nwg, cba, nbig, st);
+    gemm_mb<T, 2>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   else
-    gemm_mb<T, 4>(s, e, kind, nwg, cba, nbig, st);
+    gemm_mb<T, 4>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   if (finish) {
     const int64_t total = (int64_t)s.M * nbc * 16;
-    hipLaunchKernelGGL((gemm_finish_kernel<T>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, s, e, e.kind,
-                       (const float*)e.part);
+    const dim3 grid((unsigned)((total + 255) / 256));
+    if (ev_stop)
+      hipExtLaunchKernelGGL((gemm_finish_kernel<T>), grid, dim3(256), 0, st, nullptr, ev_stop, 0, s, e, e.kind,
+                            (const float*)e.part);
+    else
+      hipLaunchKernelGGL((gemm_finish_kernel<T>), grid, dim3(256), 0, st, s, e, e.kind, (const float*)e.part);
   }
 }
 
@@ -433,12 +445,13 @@ int gemm_pick_splits(int n_cols, int K, int dtype) {
   return s;
 }
 
-void launch_gemm(int dtype, const GemmShape& s, const GemmEpi& e, hipStream_t st) {
+void launch_gemm(int dtype, const GemmShape& s, const GemmEpi& e, hipStream_t st, hipEvent_t ev_start,
+                 hipEvent_t ev_stop) {
   if (s.M <= 0) return;
   if (dtype == DT_BF16)
-    gemm_t<bf16_t>(s, e, st);
+    gemm_t<bf16_t>(s, e, st, ev_start, ev_stop);
   else
-    gemm_t<float>(s, e, st);
+    gemm_t<float>(s, e, st, ev_start, ev_stop);
 }
 
 void launch_repack(int dtype, int kind, const void* src0, const void* src1, const void* src2, int K, int n_src,
