@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--trigram-cache", type=int, default=65536,
+                    help="entries of the trigram lookup cache measured after the headline passes (0: skip)")
     return ap.parse_args()
 
 
@@ -205,6 +207,39 @@ def main():
     spec.profile(False)
     spec.set_graph(True)
     lossless = all(out[b] == streams[b][: len(out[b])] for b in range(len(prompts)))
+
+    tri = None
+    if a.trigram_cache:
+        # trigram lookup cache: a cold pass (cache filled only by the prompt and
+        # the run itself) and a warm pass (the same run again, so every draft
+        # trigram is cached); both must reproduce the stream above exactly
+        spec.trigram_cache(a.trigram_cache)
+        tri = {"entries": a.trigram_cache}
+        for label in ("cold", "warm"):
+            first = spec.prefill(prompts)
+            out2 = [[int(t)] for t in first]
+            for _ in range(a.warmup):
+                toks, n, _ = spec.step()
+                for b in range(len(prompts)):
+                    out2[b] += [int(x) for x in toks[b, : n[b]]]
+            l0, h0 = spec.trigram_stats()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            acc2 = 0
+            for _ in range(a.steps):
+                toks, n, _ = spec.step()
+                acc2 += int(n.sum())
+                for b in range(len(prompts)):
+                    out2[b] += [int(x) for x in toks[b, : n[b]]]
+            torch.cuda.synchronize()
+            dt2 = time.perf_counter() - t0
+            l1, h1 = spec.trigram_stats()
+            same = all(out2[b] == out[b][: len(out2[b])] for b in range(len(prompts)))
+            tri[label] = {"tokens_per_s": round(acc2 / dt2, 2), "ms_per_step": round(dt2 / a.steps * 1e3, 4),
+                          "lookups": l1 - l0, "hits": h1 - h0,
+                          "hit_rate": round((h1 - h0) / max(l1 - l0, 1), 4), "same_stream": same}
+            log(f"[bench] trigram cache {label}: {tri[label]}")
+        spec.trigram_cache(0)
     value = accepted / dt
     gemm_gbs = prof.gemm_verify_bytes / (prof.ms_gemm_verify * 1e-3) / 1e9
     verify_gbs = prof.verify_bytes / (prof.ms_verify * 1e-3) / 1e9
@@ -273,6 +308,7 @@ def main():
         "tail_ms": round(prof.ms_tail / prof.steps, 4),
         "accept_len_mean": round(accepted / a.steps / len(prompts), 4),
         "lossless_vs_greedy": lossless,
+        "trigram_cache": tri,
         "greedy_tokens_per_s": round(ar_rate, 2),
         "speedup_vs_greedy": round(value / ar_rate, 3),
         "cpu_baseline": cpu,

@@ -183,6 +183,28 @@ chimera_status chimera_profile_read(chimera_ctx* ctx, chimera_profile* out);
  * stream); 0 launches every kernel individually.  Results are identical. */
 chimera_status chimera_set_graph(chimera_ctx* ctx, int32_t enable);
 
+/* Trigram lookup cache (Sec. 4.1.1: a fixed-size dictionary of trigram
+ * encoder outputs with least-recently-used replacement).  The cache holds
+ * n_entries outputs of Eq. 2 (float32, d_model each) in 8-way sets keyed by
+ * the trigram's three token ids.  While attached:
+ *  - prefill inserts the prompt's trigrams;
+ *  - every draft level looks its trigram rows up first, and the trigram MLP
+ *    is skipped when every row hits;
+ *  - the rows it does compute are inserted, evicting a set's least recently
+ *    used entry.
+ * It is exact memoization: tokens, trees and logits are bit-identical with
+ * and without it.  Evicted entries are dropped; a later miss recomputes
+ * them.  The arena (device memory of chimera_trigram_cache_bytes, 256-byte
+ * aligned) is owned by the caller and borrowed until it is detached
+ * (arena == NULL) or the context is freed.  n_entries: a positive multiple of
+ * 8.  Needs a draft (n_nodes > 1) and vocab < 2^21 - 1; CHIMERA_EINVAL
+ * otherwise, CHIMERA_ENOMEM if the arena is too small.  Attaching empties the
+ * cache and synchronises the device. */
+chimera_status chimera_trigram_cache_bytes(const chimera_model* m, int32_t n_entries, int64_t* bytes);
+chimera_status chimera_set_trigram_cache(chimera_ctx* ctx, void* arena, int64_t arena_bytes, int32_t n_entries);
+/* Cumulative draft-level trigram lookups and hits since the cache was attached. */
+chimera_status chimera_trigram_cache_stats(chimera_ctx* ctx, int64_t* lookups, int64_t* hits);
+
 /* Test hook: y[M][N] (float32, host) = x[M][K] @ w[K][N] through the
  * repack and GEMM kernels of `dtype`, on device buffers the call allocates
  * and frees itself.  x and w are host arrays of that dtype. */

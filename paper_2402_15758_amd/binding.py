@@ -63,6 +63,9 @@ _PROTOS = {
     "chimera_set_graph": [P, I32],
     "chimera_profile_read": [P, ctypes.POINTER(chimera_profile)],
     "chimera_debug_gemm": [I32, P, P, I32, I32, I32, ctypes.POINTER(ctypes.c_float)],
+    "chimera_trigram_cache_bytes": [P, I32, PI64],
+    "chimera_set_trigram_cache": [P, P, I64, I32],
+    "chimera_trigram_cache_stats": [P, PI64, PI64],
 }
 
 
@@ -182,6 +185,22 @@ def chimera_profile_read(ctx: int) -> chimera_profile:
 
 def chimera_debug_gemm(dtype: int, x_ptr: int, w_ptr: int, M: int, N: int, K: int, y_ptr: int):
     _check(lib().chimera_debug_gemm(dtype, x_ptr, w_ptr, M, N, K, ctypes.cast(y_ptr, ctypes.POINTER(ctypes.c_float))))
+
+
+def chimera_trigram_cache_bytes(model: int, n_entries: int) -> int:
+    out = I64()
+    _check(lib().chimera_trigram_cache_bytes(model, n_entries, ctypes.byref(out)))
+    return out.value
+
+
+def chimera_set_trigram_cache(ctx: int, arena_ptr, arena_bytes: int, n_entries: int):
+    _check(lib().chimera_set_trigram_cache(ctx, arena_ptr, arena_bytes, n_entries))
+
+
+def chimera_trigram_cache_stats(ctx: int):
+    lookups, hits = I64(), I64()
+    _check(lib().chimera_trigram_cache_stats(ctx, ctypes.byref(lookups), ctypes.byref(hits)))
+    return lookups.value, hits.value
 
 
 def chimera_ctx_free(ctx: int):

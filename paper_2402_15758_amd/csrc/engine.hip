@@ -182,6 +182,9 @@ struct chimera_ctx {
   int* v_pos = nullptr;
   int64_t* v_kvoff = nullptr;
   int64_t* rowtab = nullptr;  // [B][TREE_ATTN_TAIL_ROWS]: tail-pass staged rows of the current verify pass
+  // trigram lookup cache (attached by chimera_set_trigram_cache; hit/miss/stats live in this arena)
+  TriCache tri;
+  bool tri_on = false;
   int* v_qrow = nullptr;
   // draft workspaces
   void* tri_in = nullptr;
@@ -276,7 +279,7 @@ struct Gemm {
   bool timed;  // record events around the launch (verify GEMMs while profiling)
 
   void run(const void* X, int x_mtiles, int M, const void* W, int N, int K, GemmEpi e, int nb_off = 0,
-           int nb_count = 0) const {
+           int nb_count = 0, const int* skip = nullptr) const {
     GemmShape s;
     s.X = X;
     s.x_mtiles = x_mtiles;
@@ -286,6 +289,7 @@ struct Gemm {
     s.K = K;
     s.nb_off = nb_off;
     s.nb_count = nb_count;
+    s.skip = skip;
     const int cols = nb_count ? nb_count * 16 : N;
     s.splits = gemm_pick_splits(cols, K, c->m->dt);
     const int tiles_read = M <= 16 ? 1 : (M <= 32 ? 2 : 4 * ((M + 63) / 64));
@@ -460,16 +464,24 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
   for (int k = 0; k < K; ++k) {
     const int Mk = k == 0 ? B * (2 * (K + 1) + 1) : B;
     launch_draft_rows(dt, s, m->embed, k, c->tri_in, c->mt_d, c->d_pos, c->d_kvoff, c->d_qrow, st);
+    // trigram encoder (Eq. 2); with the cache, hits fill their rows and the MLP
+    // launches do nothing when every row hit
+    const int* tri_skip = nullptr;
+    if (c->tri_on) {
+      launch_tri_lookup(s, c->tri, k, c->htri, st);
+      tri_skip = c->tri.miss;
+    }
     GemmEpi e1;
     e1.kind = EPI_SILU;
     e1.out_t = c->tri_a;
     e1.o_mtiles = c->mt_d;
-    g.run(c->tri_in, c->mt_d, Mk, m->tri_w1, d, 3 * d, e1);
+    g.run(c->tri_in, c->mt_d, Mk, m->tri_w1, d, 3 * d, e1, 0, 0, tri_skip);
     GemmEpi e2;
     e2.kind = EPI_F32;
     e2.out_f = c->htri;
     e2.ldo = d;
-    g.run(c->tri_a, c->mt_d, Mk, m->tri_w2, d, d, e2);
+    g.run(c->tri_a, c->mt_d, Mk, m->tri_w2, d, d, e2, 0, 0, tri_skip);
+    if (c->tri_on) launch_tri_insert(s, c->tri, k, 0, 0, 0, c->htri, st);
     launch_rmsnorm(dt, c->htri, nullptr, 0, m->enc.attn_norm, c->un, c->mt_d, nullptr, Mk, d, cf.rms_eps, 0,
                    k == 0 ? c->pro_h : nullptr, B, B + B * (K + 1), st);
     GemmEpi eq;
@@ -615,6 +627,9 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   c->part_o = a.arr<float>(qrows * H * c->G * hd);
   c->part_ml = a.arr<float>(qrows * H * c->G * 2);
   c->rowtab = a.arr<int64_t>(B * TREE_ATTN_TAIL_ROWS);
+  c->tri.hit = a.arr<int>(Md);
+  c->tri.miss = a.arr<int>(1);
+  c->tri.stats = a.arr<unsigned long long>(2);
   c->v_pos = a.arr<int>(Mv);
   c->v_kvoff = a.arr<int64_t>(Mv);
   c->v_qrow = a.arr<int>(Mv);
@@ -999,6 +1014,8 @@ chimera_status chimera_ctx_create(chimera_model* m, chimera_kv* kv, const int32_
       upload_meta(c->chain, cp, cr, cd, ca);
       HIPCK(hipMemcpy(c->s_k_dev, c->s_k.data(), 8 * sizeof(int), hipMemcpyHostToDevice));
       HIPCK(hipMemset(c->inject_on, 0, sizeof(int)));
+      HIPCK(hipMemset(c->tri.miss, 0, sizeof(int)));
+      HIPCK(hipMemset(c->tri.stats, 0, 2 * sizeof(unsigned long long)));
       HIPCK(hipMemset(c->n, 0, sizeof(int) * c->B));
       HIPCK(hipMemset(c->tok, 0, sizeof(int) * (size_t)c->B * c->tok_stride));
       HIPCK(hipHostMalloc((void**)&c->host_out, sizeof(int) * 3 * (size_t)c->B * (c->K + 1)));
@@ -1059,6 +1076,7 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
         e2.out_f = ctx->htri + (size_t)M * d;
         e2.ldo = d;
         g.run(ctx->tri_a, ctx->mt_d, M, m->tri_w2, d, d, e2);
+        if (ctx->tri_on) launch_tri_insert(s, ctx->tri, 0, b, p0, M, ctx->htri + (size_t)M * d, st);
         launch_rmsnorm(dt, ctx->htri, nullptr, 0, m->enc.attn_norm, ctx->un, ctx->mt_d, nullptr, 2 * M, d, cf.rms_eps,
                        0, ctx->hl_rm, 0, M, st);
         GemmEpi ekv;
@@ -1354,6 +1372,61 @@ chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, i
       throw;
     }
     cleanup();
+  });
+}
+
+static int64_t tri_header_bytes(int64_t n_entries) {
+  const int64_t h = n_entries * (int64_t)(sizeof(unsigned long long) + sizeof(unsigned int)) + 256;
+  return (h + 255) / 256 * 256;
+}
+
+chimera_status chimera_trigram_cache_bytes(const chimera_model* m, int32_t n_entries, int64_t* bytes) {
+  return guard([&] {
+    REQUIRE(m != nullptr && bytes != nullptr, CHIMERA_EINVAL, "null argument");
+    REQUIRE(n_entries >= TRI_WAYS && n_entries % TRI_WAYS == 0, CHIMERA_EINVAL,
+            "n_entries must be a positive multiple of 8");
+    *bytes = tri_header_bytes(n_entries) + (int64_t)n_entries * m->cfg.d_model * (int64_t)sizeof(float);
+  });
+}
+
+chimera_status chimera_set_trigram_cache(chimera_ctx* ctx, void* arena, int64_t arena_bytes, int32_t n_entries) {
+  return guard([&] {
+    check_ctx(ctx);
+    drop_graph(ctx);
+    if (arena == nullptr) {
+      ctx->tri_on = false;
+      return;
+    }
+    REQUIRE(ctx->K > 0, CHIMERA_EINVAL, "the trigram cache needs a draft (tree with more than one node)");
+    REQUIRE(ctx->m->cfg.vocab < (1 << 21) - 1, CHIMERA_EINVAL, "vocab too large for the trigram key");
+    REQUIRE(n_entries >= TRI_WAYS && n_entries % TRI_WAYS == 0, CHIMERA_EINVAL,
+            "n_entries must be a positive multiple of 8");
+    const int64_t hb = tri_header_bytes(n_entries);
+    const int64_t need = hb + (int64_t)n_entries * ctx->m->cfg.d_model * (int64_t)sizeof(float);
+    REQUIRE(arena_bytes >= need, CHIMERA_ENOMEM, "trigram cache arena too small");
+    REQUIRE(((uintptr_t)arena & 255) == 0, CHIMERA_EINVAL, "arena must be 256-byte aligned");
+    char* p = (char*)arena;
+    ctx->tri.keys = (unsigned long long*)p;
+    ctx->tri.stamps = (unsigned int*)(p + (size_t)n_entries * sizeof(unsigned long long));
+    ctx->tri.clock = (unsigned int*)(p + (size_t)n_entries * (sizeof(unsigned long long) + sizeof(unsigned int)));
+    ctx->tri.vals = (float*)(p + hb);
+    ctx->tri.n_sets = n_entries / TRI_WAYS;
+    HIPCK(hipMemset(arena, 0, (size_t)hb));  // keys (empty), stamps, clock; values are written on insert
+    HIPCK(hipMemset(ctx->tri.miss, 0, sizeof(int)));
+    HIPCK(hipMemset(ctx->tri.stats, 0, 2 * sizeof(unsigned long long)));
+    HIPCK(hipDeviceSynchronize());
+    ctx->tri_on = true;
+  });
+}
+
+chimera_status chimera_trigram_cache_stats(chimera_ctx* ctx, int64_t* lookups, int64_t* hits) {
+  return guard([&] {
+    check_ctx(ctx);
+    REQUIRE(lookups != nullptr && hits != nullptr, CHIMERA_EINVAL, "null argument");
+    unsigned long long st[2] = {0, 0};
+    HIPCK(hipMemcpy(st, ctx->tri.stats, sizeof(st), hipMemcpyDeviceToHost));
+    *lookups = (int64_t)st[0];
+    *hits = (int64_t)st[1];
   });
 }
 

@@ -44,6 +44,7 @@ struct GemmEpi {
 };
 
 struct GemmShape {
+  const int* skip = nullptr;  // optional: the launch does nothing when *skip == 0 (device int)
   const void* X = nullptr;  // tiled activations
   int x_mtiles = 0;         // 16-row tiles of X's buffer
   int M = 0;
@@ -188,5 +189,29 @@ void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, in
                          void* tri_in, int tri_mtiles, int* enc_pos, int64_t* enc_kvoff, int* enc_qrow, int* pf_n,
                          hipStream_t st);
 // Prefill end: pending token, h_last, committed length and tokens.
+// ---- trigram lookup cache (exact memoization of the trigram encoder) -------
+// Set-associative with TRI_WAYS ways and least-recently-used replacement.
+// Key of the trigram ending at position p: token ids + 1 of positions p-2,
+// p-1, p (0 before the sequence start) packed into 21 bits each.
+constexpr int TRI_WAYS = 8;
+struct TriCache {
+  unsigned long long* keys = nullptr;   // [n_sets][TRI_WAYS], 0 = empty
+  unsigned int* stamps = nullptr;       // [n_sets][TRI_WAYS], last use
+  float* vals = nullptr;                // [n_sets][TRI_WAYS][d]: trigram encoder outputs
+  unsigned int* clock = nullptr;        // [1]
+  int n_sets = 0;
+  int* hit = nullptr;                   // [rows]: 1 = row filled from the cache or needs no trigram
+  int* miss = nullptr;                  // [1]: rows left for the trigram MLP (0 skips it)
+  unsigned long long* stats = nullptr;  // [2]: lookups, hits
+};
+// Draft level `level`: look up the trigram rows of draft_rows (query rows and
+// committed trigram rows), copy hits into htri rows [r][d].
+void launch_tri_lookup(const StepState& s, const TriCache& c, int level, float* htri, hipStream_t st);
+// Insert the rows the MLP computed: draft level (prefill_M = 0, rows as in
+// draft_rows, values htri[r]) or a prefill chunk of sequence b at positions
+// p0 .. p0+prefill_M-1 (values vals[i]).  Resets the miss count.
+void launch_tri_insert(const StepState& s, const TriCache& c, int level, int b, int p0, int prefill_M,
+                       const float* vals, hipStream_t st);
+
 void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,
                            hipStream_t st);

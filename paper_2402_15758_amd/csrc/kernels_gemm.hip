@@ -314,6 +314,7 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
 template <typename T, int MB, int CBA>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const GemmEpi e, int kind, int nbig) {
   constexpr int PF = MB == 1 ? 4 : 3;
+  if (sh.skip && *sh.skip == 0) return;
   __shared__ f32x4 red[4 * MB * CBA * 64];
   const int kblocks = sh.K / (4 * ET<T>::VEC);
   const int kps = kblocks / sh.splits;
@@ -343,6 +344,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const Gem
 // per output element of the launch's column blocks).
 template <typename T>
 __global__ void gemm_finish_kernel(const GemmShape sh, const GemmEpi e, int kind, const float* __restrict__ part) {
+  if (sh.skip && *sh.skip == 0) return;
   const int nbc = sh.nb_count ? sh.nb_count : sh.N / 16;
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t total = (int64_t)sh.M * nbc * 16;

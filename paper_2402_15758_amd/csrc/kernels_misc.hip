@@ -508,6 +508,125 @@ __global__ void prefill_rows_kernel(StepState s, const T* E, int b, int p0, int 
   trigram_row<T>(s, E, b, p, tri_in, tri_mtiles, i);
 }
 
+// ---------------------------------------------------------------------------
+// Trigram lookup cache
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ unsigned long long tri_key(const StepState& s, int b, int p) {
+  auto t = [&](int q) -> unsigned long long {
+    return q >= 0 ? (unsigned long long)(s.tok[(int64_t)b * s.tok_stride + q] + 1) : 0ull;
+  };
+  return (t(p - 2) << 42) | (t(p - 1) << 21) | t(p);
+}
+
+__device__ __forceinline__ int tri_set(unsigned long long key, int n_sets) {
+  unsigned long long z = key + 0x9e3779b97f4a7c15ull;  // SplitMix64 finalizer as the set hash
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  z = z ^ (z >> 31);
+  return (int)(z % (unsigned long long)n_sets);
+}
+
+// Row r of a draft level (the row order of draft_rows_kernel): the trigram's
+// sequence and end position, or false for rows without a trigram.
+__device__ __forceinline__ bool draft_tri_row(const StepState& s, int level, int r, int& b, int& p) {
+  const int B = s.B, K1 = s.K + 1;
+  if (r < B) {
+    b = r;
+    p = s.n[b] + level;
+    return true;
+  }
+  if (r < B + B * K1) return false;  // target-state entries
+  const int i = r - B - B * K1;
+  b = i / K1;
+  const int e = i % K1;
+  if (e >= s.pro_count[b]) return false;
+  p = s.pro_base[b] + e;
+  return true;
+}
+
+__global__ __launch_bounds__(256) void tri_lookup_kernel(StepState s, TriCache c, int level, float* __restrict__ htri) {
+  const int r = blockIdx.x, d = s.d;
+  __shared__ int way;
+  int b = 0, p = 0;
+  if (!draft_tri_row(s, level, r, b, p)) {
+    if (threadIdx.x == 0) c.hit[r] = 1;
+    return;
+  }
+  const unsigned long long key = tri_key(s, b, p);
+  const int set = tri_set(key, c.n_sets);
+  if (threadIdx.x == 0) way = -1;
+  __syncthreads();
+  if (threadIdx.x < TRI_WAYS && c.keys[(int64_t)set * TRI_WAYS + threadIdx.x] == key) way = threadIdx.x;
+  __syncthreads();
+  const int w = way;
+  if (w < 0) {
+    if (threadIdx.x == 0) {
+      c.hit[r] = 0;
+      atomicAdd(c.miss, 1);
+      atomicAdd(&c.stats[0], 1ull);
+    }
+    return;
+  }
+  const float* src = c.vals + ((int64_t)set * TRI_WAYS + w) * d;
+  for (int i = threadIdx.x; i < d; i += 256) htri[(int64_t)r * d + i] = src[i];
+  if (threadIdx.x == 0) {
+    c.hit[r] = 1;
+    c.stamps[(int64_t)set * TRI_WAYS + w] = atomicAdd(c.clock, 1u) + 1u;
+    atomicAdd(&c.stats[0], 1ull);
+    atomicAdd(&c.stats[1], 1ull);
+  }
+}
+
+// One workgroup per row.  Only the first missing row of a set inserts in a
+// launch (rows of one set never race); a key already present is left alone.
+__global__ __launch_bounds__(256) void tri_insert_kernel(StepState s, TriCache c, int level, int pb, int p0,
+                                                         int prefill_M, const float* __restrict__ vals) {
+  const int r = blockIdx.x, d = s.d;
+  __shared__ int victim;
+  __shared__ int present;
+  if (r == 0 && threadIdx.x == 0) *c.miss = 0;  // consumed by this level's MLP launches
+  auto row_of = [&](int rr, int& b, int& p) -> bool {
+    if (prefill_M > 0) {
+      b = pb;
+      p = p0 + rr;
+      return true;
+    }
+    return draft_tri_row(s, level, rr, b, p) && c.hit[rr] == 0;
+  };
+  int b = 0, p = 0;
+  if (!row_of(r, b, p)) return;
+  const unsigned long long key = tri_key(s, b, p);
+  const int set = tri_set(key, c.n_sets);
+  for (int r2 = 0; r2 < r; ++r2) {  // an earlier row of this launch owns the set
+    int b2, p2;
+    if (row_of(r2, b2, p2) && tri_set(tri_key(s, b2, p2), c.n_sets) == set) return;
+  }
+  if (threadIdx.x == 0) {
+    int v = 0, hitw = -1;
+    unsigned int best = 0xffffffffu;
+    for (int w = 0; w < TRI_WAYS; ++w) {
+      const unsigned long long k = c.keys[(int64_t)set * TRI_WAYS + w];
+      const unsigned int st = k == 0 ? 0u : c.stamps[(int64_t)set * TRI_WAYS + w];
+      if (k == key) hitw = w;
+      if (st < best) {
+        best = st;
+        v = w;
+      }
+    }
+    victim = v;
+    present = hitw >= 0;
+  }
+  __syncthreads();
+  if (present) return;
+  const int64_t slot = (int64_t)set * TRI_WAYS + victim;
+  const float* src = vals + (int64_t)r * d;
+  for (int i = threadIdx.x; i < d; i += 256) c.vals[slot * d + i] = src[i];
+  if (threadIdx.x == 0) {
+    c.keys[slot] = key;
+    c.stamps[slot] = atomicAdd(c.clock, 1u) + 1u;
+  }
+}
+
 template <typename T>
 __global__ void prefill_finish_kernel(StepState s, int b, int n, const int* amax_row, const T* hl_row) {
   const int d = s.d;
@@ -624,6 +743,17 @@ void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, in
   else
     hipLaunchKernelGGL(prefill_rows_kernel<float>, dim3(M), dim3(256), 0, st, s, (const float*)E, b, p0, M, tokens_out,
                        (float*)tri_in, tri_mtiles, enc_pos, enc_kvoff, enc_qrow, pf_n);
+}
+
+void launch_tri_lookup(const StepState& s, const TriCache& c, int level, float* htri, hipStream_t st) {
+  const int rows = level == 0 ? s.B * (2 * (s.K + 1) + 1) : s.B;
+  hipLaunchKernelGGL(tri_lookup_kernel, dim3(rows), dim3(256), 0, st, s, c, level, htri);
+}
+
+void launch_tri_insert(const StepState& s, const TriCache& c, int level, int b, int p0, int prefill_M,
+                       const float* vals, hipStream_t st) {
+  const int rows = prefill_M > 0 ? prefill_M : (level == 0 ? s.B * (2 * (s.K + 1) + 1) : s.B);
+  hipLaunchKernelGGL(tri_insert_kernel, dim3(rows), dim3(256), 0, st, s, c, level, b, p0, prefill_M, vals);
 }
 
 void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,

@@ -156,6 +156,22 @@ class Session:
     def set_graph(self, enable: bool):
         B.chimera_set_graph(self.ctx, enable)
 
+    def trigram_cache(self, n_entries: int):
+        """Attach an empty trigram lookup cache of n_entries outputs (0 detaches)."""
+        import torch
+        if not n_entries:
+            B.chimera_set_trigram_cache(self.ctx, None, 0, 0)
+            self.tri_arena = None
+            return
+        nb = B.chimera_trigram_cache_bytes(self.model, n_entries)
+        self.tri_arena = torch.empty(nb + 256, dtype=torch.uint8, device=self.device)
+        base = (self.tri_arena.data_ptr() + 255) // 256 * 256
+        B.chimera_set_trigram_cache(self.ctx, base, nb, n_entries)
+
+    def trigram_stats(self):
+        """(lookups, hits) of draft-level trigram rows since the cache was attached."""
+        return B.chimera_trigram_cache_stats(self.ctx)
+
     def profile(self, enable: bool):
         B.chimera_profile_enable(self.ctx, enable)
 
@@ -164,6 +180,7 @@ class Session:
 
     def close(self):
         if getattr(self, "ctx", None):
+            B.chimera_set_trigram_cache(self.ctx, None, 0, 0)
             B.chimera_ctx_free(self.ctx)
             self.ctx = None
         if getattr(self, "kv", None):

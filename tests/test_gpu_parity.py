@@ -299,3 +299,54 @@ def test_small_bf16_graph_equals_eager(small):
     for (ta, na, pa, la), (tb, nb, pb, lb) in zip(*outs):
         assert np.array_equal(ta, tb) and np.array_equal(na, nb) and np.array_equal(pa, pb)
         assert np.array_equal(la.view(np.uint32), lb.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# Trigram lookup cache (Sec. 4.1.1): exact memoization of the trigram encoder
+# ---------------------------------------------------------------------------
+def _bits(a):
+    a = np.ascontiguousarray(a)
+    return a.view(np.uint32) if a.dtype == np.float32 else a
+
+
+@pytest.mark.parametrize("model,entries", [("tiny", 4096), ("tiny", 8), ("small_bf16", 4096)])
+def test_trigram_cache_is_exact(model, entries):
+    """Two passes over one prompt with and without the cache: every step's
+    tokens, tree, draft lists, accepted path and verify logits are
+    bit-identical.  The second pass repeats the first pass's trigrams, so
+    with a large cache its lookups hit; with one 8-way set entries are
+    evicted constantly."""
+    if model == "tiny":
+        cfg, tree = synth.TINY, synth.TREE_T8
+    else:
+        cfg, tree = synth.small_config(n_layers=2, d_model=512, n_heads=4, head_dim=128, d_ffn=1024, vocab=2048,
+                                       n_draft_heads=4, dtype="bf16"), synth.TREE_T32
+    log(f"trigram cache: {model}, {entries} entries, 2 passes x 10 steps")
+    s_k = [max(r[k] for r in tree if len(r) > k) + 1 for k in range(max(len(r) for r in tree))]
+    w = synth.make_weights(cfg, device="cuda")
+    prompt = synth.make_prompt(45, cfg.vocab, 11)
+    plain = make_session(cfg, w, tree, max_len=256)
+    cached = make_session(cfg, w, tree, max_len=256)
+    cached.trigram_cache(entries)
+    per_pass = []
+    for rep in range(2):
+        f1 = plain.prefill([prompt])
+        f2 = cached.prefill([prompt])
+        assert list(f1) == list(f2)
+        before = cached.trigram_stats()
+        for step in range(10):
+            a1, a2 = gpu_step(plain), gpu_step(cached)
+            for key in a1:
+                x1, x2 = a1[key], a2[key]
+                if key == "lists":  # slots past a level's candidate count are unused scratch
+                    x1 = np.concatenate([x1[:, k, :s] for k, s in enumerate(s_k)], axis=1)
+                    x2 = np.concatenate([x2[:, k, :s] for k, s in enumerate(s_k)], axis=1)
+                assert np.array_equal(_bits(x1), _bits(x2)), (rep, step, key)
+        after = cached.trigram_stats()
+        per_pass.append((after[0] - before[0], after[1] - before[1]))
+    log(f"trigram cache: (lookups, hits) per pass {per_pass}")
+    assert per_pass[0][0] > 0 and per_pass[1][0] == per_pass[0][0]
+    if entries >= 4096:
+        assert per_pass[1][1] == per_pass[1][0], "the repeated pass should hit every lookup"
+    plain.close()
+    cached.close()
