@@ -57,6 +57,9 @@ LLAMA7B = ModelConfig(n_layers=32, d_model=4096, n_heads=32, head_dim=128,
                       d_ffn=11008, vocab=32000, n_draft_heads=4, dtype="bf16")
 LLAMA13B = ModelConfig(n_layers=40, d_model=5120, n_heads=40, head_dim=128,
                        d_ffn=13824, vocab=32000, n_draft_heads=4, dtype="bf16")
+# Vicuna-33B shape (Table 1): 60 layers, d 6656, 52 heads of 128, F 17920
+VICUNA33B = ModelConfig(n_layers=60, d_model=6656, n_heads=52, head_dim=128,
+                        d_ffn=17920, vocab=32000, n_draft_heads=4, dtype="bf16")
 
 
 def small_config(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=512,
@@ -304,6 +307,8 @@ WORKLOADS = {
     # Llama-13B shape, 1024-token prompt, p = 0.5 and p = 0.8
     "llama13b_p1024_a05": Workload("llama13b_p1024_a05", LLAMA13B, "T64", 1, 1024, 256, (0.5,)),
     "llama13b_p1024_a08": Workload("llama13b_p1024_a08", LLAMA13B, "T64", 1, 1024, 256, (0.8,)),
+    # Vicuna-33B shape, 512-token prompt, T64, p = 0.7
+    "vicuna33b_p512": Workload("vicuna33b_p512", VICUNA33B, "T64", 1, 512, 256, (0.7,)),
     # batch 8, ragged prompts U[256, 2048], T32, p_b ~ U[0.4, 0.9]
     "llama7b_b8": Workload("llama7b_b8", LLAMA7B, "T32", 8, 2048, 128, (0.4, 0.9), prompt_len_lo=256),
 }

@@ -124,6 +124,7 @@ def forced_lossless_run(cfg, weights, wl, steps: int, extra: int = 128):
         for b in range(B):
             streams[b] += [int(x) for x in toks[b, : n[b]]]
     ar.close()
+    del ar  # release its weight arena before the speculative session loads
     stride = max_len + 8
     ref = np.full((B, stride), -1, dtype=np.int32)
     ok = np.zeros((B, stride), dtype=np.uint8)

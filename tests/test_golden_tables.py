@@ -14,7 +14,8 @@ def _rows(tag):
 
 def test_table1_shapes():
     rows = {r[0]: tuple(int(x) for x in r[1:]) for r in _rows("table1")}
-    for name, cfg in (("Vicuna-7B", synth.LLAMA7B), ("LlaMA-2-chat-13B", synth.LLAMA13B)):
+    for name, cfg in (("Vicuna-7B", synth.LLAMA7B), ("LlaMA-2-chat-13B", synth.LLAMA13B),
+                      ("Vicuna-33B", synth.VICUNA33B)):
         layers, hidden, heads = rows[name]
         assert (cfg.n_layers, cfg.d_model, cfg.n_heads) == (layers, hidden, heads)
         assert cfg.head_dim * cfg.n_heads == hidden
