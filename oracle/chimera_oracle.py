@@ -40,7 +40,15 @@ that takes them):
   every tree branch at depth k+1;
 * greedy acceptance takes the longest root-to-node path whose every non-root
   token equals the target's argmax at its parent, then the bonus token;
-* argmax ties go to the lowest id; top-s orders by (value desc, id asc).
+* argmax ties go to the lowest id; top-s orders by (value desc, id asc);
+* typical decoding (Sec. 4.3, Sec. 5.1, T = 1): a draft node passes when the
+  target's probability of its token at its parent exceeds
+  min(eps, delta * exp(-H)), H that distribution's entropy (the paper defers
+  the rule and its thresholds to Medusa; eps = 0.09, delta = 0.3 by default);
+  the chosen node is the deepest whose whole path passes, then the highest
+  path log-probability, then the lowest index; the bonus token and the first
+  token after the prompt are sampled by the Gumbel-max trick from a
+  SplitMix64 chain keyed by (seed, sequence, position, token).
 """
 from __future__ import annotations
 
@@ -127,6 +135,86 @@ def top_s(z: np.ndarray, s: int, exclude: Optional[int] = None) -> List[int]:
     if exclude is not None:
         order = order[order != exclude]
     return [int(i) for i in order[:s]]
+
+
+# ---------------------------------------------------------------------------
+# Typical decoding (Sec. 4.3: candidates chosen by their probability under the
+# original model; Sec. 5.1: temperature T = 1)
+# ---------------------------------------------------------------------------
+_M64 = (1 << 64) - 1
+
+
+def splitmix64(x: int) -> int:
+    """One output of SplitMix64 (Steele, Lea and Flood, 2014) for state x:
+    advance by the golden-ratio increment, then two xor-shift-multiply
+    rounds and a final xor-shift."""
+    z = (x + 0x9E3779B97F4A7C15) & _M64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+    return z ^ (z >> 31)
+
+
+def sample_uniform(seed: int, b: int, pos: int, v: int) -> float:
+    """Uniform draw in (0, 1) for token v of the sample at position pos of
+    sequence b: the top 53 bits of a chain of SplitMix64 outputs, centred
+    in their interval."""
+    z = splitmix64(splitmix64(splitmix64(splitmix64(seed) ^ b) ^ pos) ^ v)
+    return ((z >> 11) + 0.5) * 2.0 ** -53
+
+
+def gumbel_sample(z: np.ndarray, seed: int, b: int, pos: int) -> int:
+    """Exact sample from softmax(z) by the Gumbel-max trick: the index of
+    the largest z_v - log(-log(u_v)) (ties to the lowest index)."""
+    g = np.array([-np.log(-np.log(sample_uniform(seed, b, pos, v))) for v in range(len(z))])
+    return argmax_lowest(np.asarray(z, dtype=np.float64) + g)
+
+
+def log_probs_entropy(z: np.ndarray):
+    """log softmax(z) and the entropy -sum p log p of softmax(z)."""
+    z = np.asarray(z, dtype=np.float64)
+    m = z.max()
+    lp = z - (m + np.log(np.exp(z - m).sum()))
+    return lp, float(-(np.exp(lp) * lp).sum())
+
+
+class Typical:
+    """Typical acceptance settings: temperature, the hard threshold eps, the
+    entropy-scaled threshold delta, and the sampler's seed."""
+
+    def __init__(self, temperature: float = 1.0, eps: float = 0.09, delta: float = 0.3, seed: int = 0):
+        self.T = float(temperature)
+        self.eps = float(eps)
+        self.delta = float(delta)
+        self.seed = int(seed)
+
+
+def typical_accept(tree: "Tree", tree_tokens: Sequence[int], logits: np.ndarray, typ: Typical, n: int,
+                   b: int = 0):
+    """Typical acceptance over a verified tree.  Node u (depth >= 1) passes
+    when p_parent(tok_u) > min(eps, delta * exp(-H_parent)) with p the
+    target distribution at temperature T; the chosen node is the deepest
+    whose whole root path passes, then the highest path log-probability,
+    then the lowest index; the bonus token is sampled from the chosen
+    node's distribution for position n + depth + 1.  Returns (path, bonus,
+    per-node pass flags, per-node token log-probabilities)."""
+    stats = [log_probs_entropy(np.asarray(r, dtype=np.float64) / typ.T) for r in logits]
+    ok = [True] * tree.n
+    lp = [0.0] * tree.n
+    for u in range(1, tree.n):
+        lpp, H = stats[tree.parent[u]]
+        thr = min(typ.eps, typ.delta * float(np.exp(-H)))
+        lp[u] = float(lpp[tree_tokens[u]])
+        ok[u] = thr <= 0.0 or lp[u] > float(np.log(thr))
+    best, best_key = 0, None
+    for u in range(tree.n):
+        if not all(ok[a] for a in tree.anc[u]):
+            continue
+        key = (tree.depth[u], sum(lp[a] for a in tree.anc[u]), -u)
+        if best_key is None or key > best_key:
+            best, best_key = u, key
+    pos = n + tree.depth[best] + 1
+    bonus = gumbel_sample(np.asarray(logits[best], dtype=np.float64) / typ.T, typ.seed, b, pos)
+    return list(tree.anc[best]), int(bonus), ok, lp
 
 
 # ---------------------------------------------------------------------------
@@ -349,7 +437,7 @@ class Decoder:
     greedy autoregressive decoding through the same cache path."""
 
     def __init__(self, oracle: Oracle, tree_ranks: Sequence[Tuple[int, ...]],
-                 forcing: Optional[Forcing] = None):
+                 forcing: Optional[Forcing] = None, typical: Optional[Typical] = None):
         self.o = oracle
         self.tree = Tree(tree_ranks)
         self.K = self.tree.levels if self.tree.n > 1 else 0
@@ -359,6 +447,7 @@ class Decoder:
         for r in self.tree.ranks[1:]:
             self.s[len(r) - 1] = max(self.s[len(r) - 1], r[-1] + 1)
         self.forcing = forcing
+        self.typical = typical
 
     # -- state -----------------------------------------------------------
     def prefill(self, prompt: Sequence[int]) -> int:
@@ -370,7 +459,11 @@ class Decoder:
         logits, h, kv = o.causal_forward(self.seq)
         self.kv = [(k.copy(), v.copy()) for k, v in kv]  # target K/V, positions 0..n-1
         self.n = n
-        self.pending = argmax_lowest(logits[-1])
+        if self.typical is not None:
+            ty = self.typical
+            self.pending = gumbel_sample(np.asarray(logits[-1], dtype=np.float64) / ty.T, ty.seed, 0, n)
+        else:
+            self.pending = argmax_lowest(logits[-1])
         self.seq.append(self.pending)
         self.h_last = h[-1].copy()
         # draft encoder memory: target-state entries 0..n-1, trigram entries 0..n-1
@@ -486,7 +579,10 @@ class Decoder:
         toks = self.assemble(lists) if tree_tokens_override is None else list(tree_tokens_override)
         logits, h, tkv = self.verify(toks)
         amax = [argmax_lowest(r) for r in logits]
-        path, bonus = self.accept(toks, amax)
+        if self.typical is not None:
+            path, bonus, _, _ = typical_accept(self.tree, toks, logits, self.typical, self.n)
+        else:
+            path, bonus = self.accept(toks, amax)
         if accept_override is not None:
             path = list(accept_override)
             bonus = amax[path[-1]]

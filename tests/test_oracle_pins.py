@@ -459,3 +459,110 @@ def test_bf16_contract_rounds_storage_points():
     prompt = list(synth.make_prompt(10, cfg.vocab, 1))
     out, _ = oracle.Decoder(o, synth.TREE_T8).generate(prompt, 12)
     assert out == o.greedy_ar(prompt, 12)
+
+
+# ---------------------------------------------------------------------------
+# Typical decoding (Sec. 4.3, Sec. 5.1)
+# ---------------------------------------------------------------------------
+def test_splitmix64_published_output():
+    # first output of SplitMix64 from state 0 (the generator's reference value)
+    assert co.splitmix64(0) == 16294208416658607535
+    assert co.splitmix64(0) == 0xE220A8397B1DCDAF
+
+
+def test_gumbel_sampling_matches_softmax():
+    """Over many positions the Gumbel-max samples follow softmax(z)."""
+    z = np.array([0.0, 1.0, 2.0, -1.0, 0.5])
+    p = np.exp(z - z.max())
+    p /= p.sum()
+    n = 6000
+    counts = np.zeros(len(z))
+    for pos in range(n):
+        counts[co.gumbel_sample(z, 7, 0, pos)] += 1
+    sd = np.sqrt(n * p * (1 - p))
+    assert np.all(np.abs(counts - n * p) <= 4.5 * sd), (counts, n * p)
+
+
+def test_sampling_is_keyed_by_sequence_position_and_seed():
+    z = np.zeros(64)
+    a = [co.gumbel_sample(z, 1, 0, pos) for pos in range(40)]
+    assert a == [co.gumbel_sample(z, 1, 0, pos) for pos in range(40)]
+    assert a != [co.gumbel_sample(z, 2, 0, pos) for pos in range(40)]
+    assert a != [co.gumbel_sample(z, 1, 1, pos) for pos in range(40)]
+
+
+def test_entropy_closed_forms():
+    for V in (2, 7, 1000):
+        lp, H = co.log_probs_entropy(np.zeros(V))
+        assert abs(H - np.log(V)) < 1e-12
+        assert np.allclose(np.exp(lp), 1.0 / V)
+    _, H = co.log_probs_entropy(np.array([300.0, 0.0, 0.0]))
+    assert H < 1e-100 + 1e-12
+
+
+def _random_tree_case(seed, V=40):
+    rng = np.random.default_rng(seed)
+    tree = co.Tree(synth.TREE_T8)
+    toks = [int(x) for x in rng.integers(0, V, size=tree.n)]
+    logits = rng.normal(0, 1.5, size=(tree.n, V))
+    return tree, toks, logits
+
+
+def test_typical_zero_thresholds_take_the_most_probable_deepest_path():
+    """With eps = delta = 0 every node passes: the chosen node is, by brute
+    force over all nodes, the deepest one with the largest path probability."""
+    for seed in range(5):
+        tree, toks, logits = _random_tree_case(seed)
+        typ = co.Typical(1.0, 0.0, 0.0, seed=3)
+        path, bonus, ok, _ = co.typical_accept(tree, toks, logits, typ, n=50)
+        assert all(ok)
+        best, best_key = None, None
+        for u in range(tree.n):
+            prob = 1.0
+            for a in tree.anc[u][1:]:
+                q = np.exp(logits[tree.parent[a]] - logits[tree.parent[a]].max())
+                prob *= q[toks[a]] / q.sum()
+            key = (tree.depth[u], prob)
+            if best_key is None or key > best_key:
+                best, best_key = u, key
+        assert path == list(tree.anc[best])
+        assert bonus == co.gumbel_sample(logits[best], 3, 0, 50 + tree.depth[best] + 1)
+
+
+def test_typical_unreachable_threshold_keeps_only_the_root():
+    tree, toks, logits = _random_tree_case(11)
+    typ = co.Typical(1.0, 1.5, 1e9, seed=5)
+    path, bonus, ok, _ = co.typical_accept(tree, toks, logits, typ, n=9)
+    assert path == [0] and not any(ok[1:])
+    assert bonus == co.gumbel_sample(logits[0], 5, 0, 10)
+
+
+def test_typical_acceptance_is_monotone_in_the_thresholds():
+    """Raising eps or delta never lets more nodes pass."""
+    for seed in range(4):
+        tree, toks, logits = _random_tree_case(20 + seed, V=6)
+        prev = None
+        for eps, delta in [(0.0, 0.0), (0.05, 0.1), (0.09, 0.3), (0.2, 0.6), (0.5, 2.0)]:
+            _, _, ok, _ = co.typical_accept(tree, toks, logits, co.Typical(1.0, eps, delta), n=0)
+            if prev is not None:
+                assert all(p or not q for p, q in zip(prev, ok))
+            prev = ok
+
+
+def test_typical_sampling_without_draft_is_plain_sampling(orc):
+    """With no draft (a one-node tree) typical decoding is autoregressive
+    sampling: every token is the Gumbel-max sample of a plain causal forward
+    at its position."""
+    prompt = list(synth.make_prompt(9, CFG.vocab, 4))
+    dec = oracle.Decoder(orc, (), typical=co.Typical(1.0, seed=9))
+    out = [dec.prefill(prompt)]
+    for _ in range(5):
+        out += dec.step()["new_tokens"]
+    seq = list(prompt)
+    want = []
+    for _ in range(6):
+        logits, _, _ = orc.causal_forward(seq)
+        t = co.gumbel_sample(logits[-1], 9, 0, len(seq))
+        want.append(t)
+        seq.append(t)
+    assert out == want
