@@ -47,6 +47,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--no-typical", action="store_true", help="skip the typical-decoding (T = 1) measurement")
     ap.add_argument("--trigram-cache", type=int, default=65536,
                     help="entries of the trigram lookup cache measured after the headline passes (0: skip)")
     return ap.parse_args()
@@ -264,6 +265,39 @@ def main():
             cpu = cpu_baseline(wl, weights, prompts[0], accepted / a.steps)
         except MemoryError:
             cpu = None
+    typ = None
+    if not a.no_typical:
+        # typical decoding at T = 1 (sampling, not lossless): accepted length and
+        # rate of the speculative session, against plain sampling (no draft)
+        spec.set_decoding(True, 1.0, 0.09, 0.3, seed=17)
+        ar.set_decoding(True, 1.0, 0.09, 0.3, seed=17)
+        spec.prefill(prompts)
+        for _ in range(a.warmup):
+            spec.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        acc3 = 0
+        for _ in range(a.steps):
+            _, n, _ = spec.step()
+            acc3 += int(n.sum())
+        torch.cuda.synchronize()
+        dt3 = time.perf_counter() - t0
+        ar.prefill(prompts)
+        for _ in range(a.warmup):
+            ar.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(a.steps):
+            ar.step()
+        torch.cuda.synchronize()
+        dt4 = time.perf_counter() - t0
+        spec.set_decoding(False)
+        ar.set_decoding(False)
+        typ = {"temperature": 1.0, "eps": 0.09, "delta": 0.3,
+               "tokens_per_s": round(acc3 / dt3, 2), "accept_len_mean": round(acc3 / a.steps / len(prompts), 3),
+               "sampling_tokens_per_s": round(a.steps * len(prompts) / dt4, 2),
+               "speedup_vs_sampling": round((acc3 / dt3) / (a.steps * len(prompts) / dt4), 3)}
+        log(f"[bench] typical decoding: {typ}")
     line = {
         "metric": "accepted tokens/sec at batch 1 (Llama-7B-shape bf16); verify-pass % of HBM peak",
         "value": round(value, 2),
@@ -309,6 +343,7 @@ def main():
         "accept_len_mean": round(accepted / a.steps / len(prompts), 4),
         "lossless_vs_greedy": lossless,
         "trigram_cache": tri,
+        "typical_decoding": typ,
         "greedy_tokens_per_s": round(ar_rate, 2),
         "speedup_vs_greedy": round(value / ar_rate, 3),
         "cpu_baseline": cpu,

@@ -183,6 +183,27 @@ chimera_status chimera_profile_read(chimera_ctx* ctx, chimera_profile* out);
  * stream); 0 launches every kernel individually.  Results are identical. */
 chimera_status chimera_set_graph(chimera_ctx* ctx, int32_t enable);
 
+/* Verification rule (Sec. 4.3; Sec. 5.1 tests greedy and typical decoding at
+ * T = 1).  CHIMERA_DECODE_GREEDY (the default) accepts the longest path of
+ * target argmax tokens and is lossless against greedy decoding.
+ * CHIMERA_DECODE_TYPICAL selects candidates by their probability under the
+ * target at the given temperature:
+ *  - a draft node passes when p_parent(token) > min(eps, delta * exp(-H)),
+ *    H the entropy of the parent's distribution (the rule the paper takes
+ *    from Medusa, which it does not spell out; 0.09 and 0.3 are the usual
+ *    values);
+ *  - the deepest node whose whole path passes is accepted (ties: higher path
+ *    log-probability, then lower node id);
+ *  - the bonus token, and the first token after a prompt, are sampled by the
+ *    Gumbel-max trick.  u_v uses the top 53 bits of
+ *    SplitMix64(SplitMix64(SplitMix64(SplitMix64(seed) ^ b) ^ position) ^ v),
+ *    b the sequence, position the token's position, v the token id.
+ * Not lossless: the stream is a sample, reproducible from the seed.
+ * Takes effect from the next prefill or step. */
+enum { CHIMERA_DECODE_GREEDY = 0, CHIMERA_DECODE_TYPICAL = 1 };
+chimera_status chimera_set_decoding(chimera_ctx* ctx, int32_t mode, float temperature, float eps, float delta,
+                                    uint64_t seed);
+
 /* Trigram lookup cache (Sec. 4.1.1: a fixed-size dictionary of trigram
  * encoder outputs with least-recently-used replacement).  The cache holds
  * n_entries outputs of Eq. 2 (float32, d_model each) in 8-way sets keyed by

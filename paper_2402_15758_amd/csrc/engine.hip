@@ -185,6 +185,13 @@ struct chimera_ctx {
   // trigram lookup cache (attached by chimera_set_trigram_cache; hit/miss/stats live in this arena)
   TriCache tri;
   bool tri_on = false;
+  // decoding: greedy, or typical acceptance with sampling (chimera_set_decoding)
+  int typical = 0;
+  float temperature = 1.f, t_eps = 0.09f, t_delta = 0.3f;
+  unsigned long long t_seed = 0;
+  double* t_lse = nullptr;  // [Mv]
+  double* t_H = nullptr;    // [Mv]
+  int* t_sample = nullptr;  // [Mv]
   int* v_qrow = nullptr;
   // draft workspaces
   void* tri_in = nullptr;
@@ -450,6 +457,14 @@ StepState make_state(chimera_ctx* c) {
   s.v_pos = c->v_pos;
   s.v_kvoff = c->v_kvoff;
   s.v_qrow = c->v_qrow;
+  s.typical = c->typical;
+  s.inv_T = 1.f / c->temperature;
+  s.eps = c->t_eps;
+  s.delta = c->t_delta;
+  s.logits = c->logits;
+  s.t_lse = c->t_lse;
+  s.t_H = c->t_H;
+  s.t_sample = c->t_sample;
   return s;
 }
 
@@ -627,6 +642,9 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   c->part_o = a.arr<float>(qrows * H * c->G * hd);
   c->part_ml = a.arr<float>(qrows * H * c->G * 2);
   c->rowtab = a.arr<int64_t>(B * TREE_ATTN_TAIL_ROWS);
+  c->t_lse = a.arr<double>(Mv);
+  c->t_H = a.arr<double>(Mv);
+  c->t_sample = a.arr<int>(Mv);
   c->tri.hit = a.arr<int>(Md);
   c->tri.miss = a.arr<int>(1);
   c->tri.stats = a.arr<unsigned long long>(2);
@@ -1100,7 +1118,11 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
           el.out_f = ctx->logits;
           el.ldo = V;
           g.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
-          launch_argmax(ctx->logits + (size_t)(M - 1) * V, 1, V, ctx->amax, st);
+          if (ctx->typical)  // the first generated token is sampled at position n
+            launch_typical_stats(ctx->logits + (size_t)(M - 1) * V, 1, V, 1, b, nullptr, nullptr, n,
+                                 1.f / ctx->temperature, ctx->t_seed, ctx->t_lse, ctx->t_H, ctx->amax, st);
+          else
+            launch_argmax(ctx->logits + (size_t)(M - 1) * V, 1, V, ctx->amax, st);
           const char* last = (const char*)ctx->hl_rm + (size_t)(M - 1) * d * m->es;
           launch_prefill_finish(dt, s, b, n, ctx->amax, last, st);
         }
@@ -1160,7 +1182,11 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
       el.out_f = ctx->logits;
       el.ldo = V;
       gq.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
-      launch_argmax(ctx->logits, M, V, ctx->amax, q);
+      if (ctx->typical)
+        launch_typical_stats(ctx->logits, M, V, ctx->N, 0, ctx->n, ctx->tree.depth, -1, 1.f / ctx->temperature,
+                             ctx->t_seed, ctx->t_lse, ctx->t_H, ctx->t_sample, q);
+      else
+        launch_argmax(ctx->logits, M, V, ctx->amax, q);
       if (ctx->prof) HIPCK(hipEventRecord(ctx->e_verify, q));
       launch_accept(dt, s, q);
       launch_compact(dt, s, kv->pool, cf.n_layers, kv->layer_stride, q);
@@ -1372,6 +1398,23 @@ chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, i
       throw;
     }
     cleanup();
+  });
+}
+
+chimera_status chimera_set_decoding(chimera_ctx* ctx, int32_t mode, float temperature, float eps, float delta,
+                                    uint64_t seed) {
+  return guard([&] {
+    check_ctx(ctx);
+    REQUIRE(mode == CHIMERA_DECODE_GREEDY || mode == CHIMERA_DECODE_TYPICAL, CHIMERA_EINVAL, "decoding mode");
+    if (mode == CHIMERA_DECODE_TYPICAL)
+      REQUIRE(temperature > 0.f && eps >= 0.f && delta >= 0.f, CHIMERA_EINVAL,
+              "typical decoding needs temperature > 0, eps >= 0, delta >= 0");
+    drop_graph(ctx);
+    ctx->typical = mode == CHIMERA_DECODE_TYPICAL;
+    ctx->temperature = mode == CHIMERA_DECODE_TYPICAL ? temperature : 1.f;
+    ctx->t_eps = eps;
+    ctx->t_delta = delta;
+    ctx->t_seed = seed;
   });
 }
 

@@ -161,7 +161,23 @@ struct StepState {
   int* v_pos;               // [B*N]
   int64_t* v_kvoff;         // [B*N]
   int* v_qrow;              // [B*N]
+  // typical decoding (typical != 0): the verify logits, their per-row
+  // log-sum-exp and entropy at temperature 1 / inv_T, and each row's sample
+  int typical;
+  float inv_T, eps, delta;
+  const float* logits;      // [B*N][V]
+  const double* t_lse;      // [B*N]
+  const double* t_H;        // [B*N]
+  const int* t_sample;      // [B*N]
 };
+// Per row r of logits [rows][V]: at temperature 1 / inv_T, lse = log sum_v
+// exp(z_v), H = the entropy of softmax(z), and sample = the Gumbel-max sample
+// (argmax_v z_v - log(-log(u_v)), u_v from the SplitMix64 chain keyed by
+// (seed, sequence, position, v)) for sequence b0 + r / N at position
+// n_b[b] + depth[r % N] + 1, or at fixed_pos when fixed_pos >= 0.
+void launch_typical_stats(const float* logits, int rows, int V, int N, int b0, const int* n_b, const int* depth,
+                          int fixed_pos, float inv_T, unsigned long long seed, double* lse, double* H, int* sample,
+                          hipStream_t st);
 void launch_argmax(const float* logits, int M, int V, int* amax, hipStream_t st);
 // scratch: [B][32][8] values and ids
 void launch_topk(const float* logits, const StepState& s, int level, float* scratch_v, int* scratch_i,

@@ -327,26 +327,72 @@ __global__ void tree_setup_kernel(StepState s) {
 }
 
 // Greedy acceptance, one wave per sequence, lane = tree node.
+__device__ __forceinline__ double readlane_f64(double x, int lane) {
+  const unsigned long long u = (unsigned long long)__double_as_longlong(x);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)u, lane);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(u >> 32), lane);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
 __global__ void accept_kernel(StepState s) {
   const int b = blockIdx.x, u = threadIdx.x;
   const bool valid = u < s.N;
   const int row = b * s.N + (valid ? u : 0);
-  const int a_u = s.amax[row];
   const int tok_u = s.tree_tok[row];
   const int par = valid ? s.t_parent[u] : -1;
-  const int a_par = par >= 0 ? s.amax[b * s.N + par] : -1;
-  const bool good = valid && (u == 0 || tok_u == a_par);
-  const unsigned long long goodmask = __ballot(good);
   const unsigned long long anc = valid ? s.t_anc[u] : 0ull;
-  const bool acc = valid && ((anc & ~goodmask) == 0ull);
-  int key = acc ? s.t_depth[u] : -1;
+  const int dep = s.t_depth[valid ? u : 0];
+  int v, bonus;
+  if (!s.typical) {
+    // greedy: every non-root token equals the target argmax at its parent;
+    // the deepest such node (unique: siblings are distinct)
+    const int a_u = s.amax[row];
+    const int a_par = par >= 0 ? s.amax[b * s.N + par] : -1;
+    const bool good = valid && (u == 0 || tok_u == a_par);
+    const unsigned long long goodmask = __ballot(good);
+    const bool acc = valid && ((anc & ~goodmask) == 0ull);
+    int key = acc ? dep : -1;
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) key = max(key, __shfl_xor(key, m));
-  const unsigned long long vmask = __ballot(acc && s.t_depth[valid ? u : 0] == key);
-  const int v = __ffsll((long long)vmask) - 1;
+    for (int m = 32; m >= 1; m >>= 1) key = max(key, __shfl_xor(key, m));
+    const unsigned long long vmask = __ballot(acc && dep == key);
+    v = __ffsll((long long)vmask) - 1;
+    bonus = __shfl(a_u, v);
+  } else {
+    // typical: a node passes when p_parent(tok) > min(eps, delta exp(-H_parent));
+    // the deepest node whose root path passes, then the highest path
+    // log-probability, then the lowest index
+    double lp = 0.0;
+    bool ok = true;
+    if (valid && u > 0) {
+      const int pr = b * s.N + par;
+      lp = (double)(s.logits[(int64_t)pr * s.V + tok_u] * s.inv_T) - s.t_lse[pr];
+      const double thr = fmin((double)s.eps, (double)s.delta * exp(-s.t_H[pr]));
+      ok = thr <= 0.0 || lp > log(thr);
+    }
+    const unsigned long long okmask = __ballot(valid && ok);
+    const bool acc = valid && ((anc & ~okmask) == 0ull);
+    double plp = 0.0;  // path log-probability, ancestors in id (= depth) order
+    for (int x = 0; x < s.N; ++x) {
+      const double lx = readlane_f64(lp, x);
+      if ((anc >> x) & 1ull) plp += lx;
+    }
+    const unsigned long long accmask = __ballot(acc);
+    int best = 0, bd = -1;
+    double bp = 0.0;
+    for (int x = 0; x < s.N; ++x) {
+      const int dx = __builtin_amdgcn_readlane(dep, x);
+      const double px = readlane_f64(plp, x);
+      if (((accmask >> x) & 1ull) && (dx > bd || (dx == bd && px > bp))) {
+        best = x;
+        bd = dx;
+        bp = px;
+      }
+    }
+    v = best;
+    bonus = s.t_sample[b * s.N + v];
+  }
   const unsigned long long path = __shfl(anc, v);
   const int L = __popcll(path);
-  const int bonus = __shfl(a_u, v);
   const int K1 = s.K + 1;
   if (valid && ((path >> u) & 1ull)) {
     const int idx = __popcll(path & ((1ull << u) - 1ull));
@@ -356,6 +402,85 @@ __global__ void accept_kernel(StepState s) {
   if (u == 0) {
     s.out_tok[b * K1 + L - 1] = bonus;
     s.out_len[b] = L;
+  }
+}
+
+__device__ __forceinline__ unsigned long long splitmix64_d(unsigned long long x) {
+  unsigned long long z = x + 0x9e3779b97f4a7c15ull;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+// One workgroup per logits row; fp64 accumulation, fixed reduction order.
+__global__ __launch_bounds__(1024) void typical_stats_kernel(const float* __restrict__ logits, int V, int N, int b0,
+                                                             const int* __restrict__ n_b, const int* __restrict__ depth,
+                                                             int fixed_pos, float inv_T, unsigned long long seed,
+                                                             double* lse, double* Hout, int* sample) {
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const int b = b0 + r / N;
+  const int pos = fixed_pos >= 0 ? fixed_pos : n_b[b] + depth[r % N] + 1;
+  const float* l = logits + (int64_t)r * V;
+  __shared__ double red_a[1024], red_b[1024];
+  __shared__ int red_i[1024];
+  __shared__ float red_m[1024];
+  float m = -CH_INF;
+  for (int v = tid; v < V; v += 1024) m = fmaxf(m, l[v] * inv_T);
+  red_m[tid] = m;
+  __syncthreads();
+  for (int w = 512; w >= 1; w >>= 1) {
+    if (tid < w) red_m[tid] = fmaxf(red_m[tid], red_m[tid + w]);
+    __syncthreads();
+  }
+  const double mx = (double)red_m[0];
+  const unsigned long long base = splitmix64_d(splitmix64_d(splitmix64_d(seed) ^ (unsigned long long)b) ^
+                                               (unsigned long long)pos);
+  double S = 0.0, E = 0.0, best = -HUGE_VAL;
+  int bi = 0x7fffffff;
+  for (int v = tid; v < V; v += 1024) {
+    const double z = (double)(l[v] * inv_T);
+    const double e = exp(z - mx);
+    S += e;
+    E += e * (z - mx);
+    const double uu = ((double)(splitmix64_d(base ^ (unsigned long long)v) >> 11) + 0.5) * 0x1p-53;
+    const double sc = z - log(-log(uu));
+    if (sc > best) {  // ascending v per thread: ties keep the lower id
+      best = sc;
+      bi = v;
+    }
+  }
+  __syncthreads();
+  red_a[tid] = S;
+  red_b[tid] = E;
+  __syncthreads();
+  for (int w = 512; w >= 1; w >>= 1) {
+    if (tid < w) {
+      red_a[tid] = red_a[tid] + red_a[tid + w];
+      red_b[tid] = red_b[tid] + red_b[tid + w];
+    }
+    __syncthreads();
+  }
+  const double Ssum = red_a[0], Esum = red_b[0];
+  __syncthreads();
+  red_a[tid] = best;
+  red_i[tid] = bi;
+  __syncthreads();
+  for (int w = 512; w >= 1; w >>= 1) {
+    if (tid < w) {
+      const double o = red_a[tid + w];
+      const int oi = red_i[tid + w];
+      if (o > red_a[tid] || (o == red_a[tid] && oi < red_i[tid])) {
+        red_a[tid] = o;
+        red_i[tid] = oi;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const double ls = log(Ssum);
+    lse[r] = mx + ls;
+    Hout[r] = ls - Esum / Ssum;
+    sample[r] = red_i[0];
   }
 }
 
@@ -690,6 +815,13 @@ void launch_topk(const float* logits, const StepState& s, int level, float* scra
 
 void launch_tree_setup(const StepState& s, hipStream_t st) {
   hipLaunchKernelGGL(tree_setup_kernel, dim3(s.B), dim3(64), 0, st, s);
+}
+
+void launch_typical_stats(const float* logits, int rows, int V, int N, int b0, const int* n_b, const int* depth,
+                          int fixed_pos, float inv_T, unsigned long long seed, double* lse, double* H, int* sample,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(typical_stats_kernel, dim3(rows), dim3(1024), 0, st, logits, V, N, b0, n_b, depth, fixed_pos,
+                     inv_T, seed, lse, H, sample);
 }
 
 void launch_accept(int, const StepState& s, hipStream_t st) {

@@ -156,6 +156,12 @@ class Session:
     def set_graph(self, enable: bool):
         B.chimera_set_graph(self.ctx, enable)
 
+    def set_decoding(self, typical: bool, temperature: float = 1.0, eps: float = 0.09, delta: float = 0.3,
+                     seed: int = 0):
+        """Greedy verification (typical=False) or typical acceptance with sampling."""
+        B.chimera_set_decoding(self.ctx, B.CHIMERA_DECODE_TYPICAL if typical else B.CHIMERA_DECODE_GREEDY,
+                               temperature, eps, delta, seed)
+
     def trigram_cache(self, n_entries: int):
         """Attach an empty trigram lookup cache of n_entries outputs (0 detaches)."""
         import torch

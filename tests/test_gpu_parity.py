@@ -5,7 +5,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_helpers import TieLog, check_step, gpu_step, log, make_session, tau
+from gpu_helpers import TieLog, check_step, compare_lists, gpu_step, log, make_session, tau
+from oracle import chimera_oracle as co
 
 pytestmark = pytest.mark.gpu
 
@@ -350,3 +351,84 @@ def test_trigram_cache_is_exact(model, entries):
         assert per_pass[1][1] == per_pass[1][0], "the repeated pass should hit every lookup"
     plain.close()
     cached.close()
+
+
+# ---------------------------------------------------------------------------
+# Typical decoding (Sec. 4.3, Sec. 5.1, T = 1)
+# ---------------------------------------------------------------------------
+def _sample_margin(z, a, b, seed, pos):
+    """Score gap of tokens a and b in the Gumbel-max draw from z."""
+    g = lambda v: -np.log(-np.log(co.sample_uniform(seed, 0, pos, v)))
+    return abs((z[a] + g(a)) - (z[b] + g(b)))
+
+
+@pytest.mark.parametrize("tree_name", ["T8", "none"])
+def test_tiny_typical_decoding_teacher_forced(tree_name):
+    """Each step: the GPU's accepted path and bonus token follow the typical
+    rule applied to the GPU's own verify logits exactly (host mirror), and
+    the oracle's, computed from its own logits, agree up to near-ties of the
+    oracle (margin <= 2 tau * range).  The oracle then commits the GPU's
+    choice."""
+    cfg = synth.TINY
+    tree = synth.TREE_T8 if tree_name == "T8" else ()
+    typ = co.Typical(1.0, 0.09, 0.3, seed=1234)
+    log(f"typical decoding: tiny, tree {tree_name}, 8 teacher-forced steps")
+    w = synth.make_weights(cfg, device="cuda", std=0.06)
+    prompt = synth.make_prompt(30, cfg.vocab, 5)
+    sess = make_session(cfg, w, tree, max_len=128)
+    sess.set_decoding(True, typ.T, typ.eps, typ.delta, typ.seed)
+    first = int(sess.prefill([prompt])[0])
+    orc = oracle.Oracle(cfg, synth.weights_to_numpy(w))
+    dec = oracle.Decoder(orc, tree, typical=typ)
+    f_o = dec.prefill(list(prompt))
+    t = tau(cfg)
+    ties = 0
+    if first != f_o:
+        logits, _, _ = orc.causal_forward(list(prompt))
+        z = logits[-1]
+        assert _sample_margin(z, first, f_o, typ.seed, len(prompt)) <= 2 * t * (z.max() - z.min())
+        ties += 1
+        dec.pending = first
+        dec.seq[-1] = first
+    ctree = co.Tree(tree)
+    lens = []
+    for step in range(8):
+        art = gpu_step(sess)
+        L = int(art["n"][0])
+        tree_g = [int(x) for x in art["tree"][0]]
+        lg = art["logits"][0].astype(np.float64)
+        if dec.K:
+            lists_o, dz = dec.draft(chain_tokens=[int(art["lists"][0, k, 0]) for k in range(dec.K)])
+            for k in range(dec.K):
+                compare_lists(art["lists"][0, k, : dec.s[k]], lists_o[k], dz[k], t, TieLog(), False)
+        assert tree_g[0] == dec.pending
+        # the kernel against the rule on its own logits
+        path_m, bonus_m, _, _ = co.typical_accept(ctree, tree_g, lg, typ, dec.n)
+        path_g = [int(x) for x in art["path"][0, :L]]
+        bonus_g = int(art["toks"][0, L - 1])
+        assert path_g == path_m, (step, path_g, path_m)
+        assert bonus_g == bonus_m, (step, bonus_g, bonus_m)
+        # the oracle on its own logits
+        logits_o, h_o, tkv = dec.verify(tree_g)
+        rng = logits_o.max(-1) - logits_o.min(-1)
+        assert float(np.max(np.abs(lg - logits_o) / rng[:, None])) <= t
+        path_o, bonus_o, ok_o, lp_o = co.typical_accept(ctree, tree_g, logits_o, typ, dec.n)
+        if path_o != path_g:
+            # admissible only where an oracle pass decision sits on its threshold
+            near = False
+            for u in range(1, ctree.n):
+                _, H = co.log_probs_entropy(logits_o[ctree.parent[u]])
+                thr = min(typ.eps, typ.delta * np.exp(-H))
+                if abs(lp_o[u] - np.log(thr)) <= 4 * t * rng[ctree.parent[u]]:
+                    near = True
+            assert near, (step, path_g, path_o)
+            ties += 1
+        elif bonus_o != bonus_g:
+            z = logits_o[path_g[-1]]
+            pos = dec.n + ctree.depth[path_g[-1]] + 1
+            assert _sample_margin(z, bonus_g, bonus_o, typ.seed, pos) <= 2 * t * (z.max() - z.min())
+            ties += 1
+        dec.commit(path_g, bonus_g, tree_g, h_o, tkv)
+        lens.append(L)
+    log(f"typical decoding: accepted lengths {lens}, {ties} near-ties")
+    sess.close()
