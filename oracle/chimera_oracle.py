@@ -38,6 +38,13 @@ that takes them):
 * the draft runs as a chain: head k reads the encoder output at the position
   reached by the rank-0 tokens of heads 0..k-1; its top-s list is shared by
   every tree branch at depth k+1;
+* branch-conditioned drafting (the tree reading of Sec. 4.4, optional): level
+  k runs the draft once for every depth-k tree node that has children, along
+  that node's own root-to-node tokens; the encoder query of such a node sees
+  the target-state entries 0..n-1, the trigram entries 0..n-1 and the
+  trigram entries of its ancestors-or-self (the tree mask of Sec. 4.3
+  applied to the encoder), and a child of rank r takes the rank-r token of
+  its parent's own list.  On a chain-shaped tree it is chain drafting;
 * greedy acceptance takes the longest root-to-node path whose every non-root
   token equals the target's argmax at its parent, then the bonus token;
 * argmax ties go to the lowest id; top-s orders by (value desc, id asc);
@@ -437,7 +444,8 @@ class Decoder:
     greedy autoregressive decoding through the same cache path."""
 
     def __init__(self, oracle: Oracle, tree_ranks: Sequence[Tuple[int, ...]],
-                 forcing: Optional[Forcing] = None, typical: Optional[Typical] = None):
+                 forcing: Optional[Forcing] = None, typical: Optional[Typical] = None,
+                 branch: bool = False):
         self.o = oracle
         self.tree = Tree(tree_ranks)
         self.K = self.tree.levels if self.tree.n > 1 else 0
@@ -448,6 +456,11 @@ class Decoder:
             self.s[len(r) - 1] = max(self.s[len(r) - 1], r[-1] + 1)
         self.forcing = forcing
         self.typical = typical
+        self.branch = branch
+        # branch-conditioned drafting: the nodes drafted at level k are the
+        # depth-k nodes with children, in node order
+        t = self.tree
+        self.drafted = [[u for u in range(t.n) if t.depth[u] == k and u in t.parent] for k in range(self.K)]
 
     # -- state -----------------------------------------------------------
     def prefill(self, prompt: Sequence[int]) -> int:
@@ -500,6 +513,40 @@ class Decoder:
             chain.append(lst[0] if chain_tokens is None else int(chain_tokens[k]))
         return lists, (np.stack(all_logits) if all_logits else np.zeros((0, o.cfg.vocab)))
 
+    def draft_branches(self, tree_tokens: Optional[Sequence[int]] = None):
+        """Branch-conditioned drafting.  Level k runs the draft for every
+        depth-k node u with children: the trigram at position n+k is built
+        from u's own path tokens, its encoder query attends to the target
+        entries 0..n-1, the trigram entries 0..n-1 and the trigram entries of
+        u's ancestors-or-self (root first), and head k's top-s list becomes
+        the candidates of u's children.  Returns ({u: list}, {u: logits}).
+        ``tree_tokens`` (teacher forcing) supplies the path tokens instead of
+        the lists, e.g. another run's tree."""
+        o, n, t = self.o, self.n, self.tree
+        forced_path = tree_tokens is not None
+        toks = [int(x) for x in tree_tokens] if forced_path else [self.pending] + [-1] * (t.n - 1)
+        ent_k, ent_v = {}, {}
+        lists, all_logits = {}, {}
+        for k in range(self.K):
+            j = n + k
+            for u in self.drafted[k]:
+                path = t.anc[u]
+                seq = list(self.seq[: n + 1]) + [toks[a] for a in path[1:]]
+                htri = o.trigram_encode(o.trigram_inputs(seq, [j]))
+                kj, vj = o.encoder_kv(htri, np.array([j]))
+                ent_k[u], ent_v[u] = kj[0], vj[0]
+                k_mem = np.concatenate([self.llm_k[:n], self.tri_k[:n], np.stack([ent_k[a] for a in path])])
+                v_mem = np.concatenate([self.llm_v[:n], self.tri_v[:n], np.stack([ent_v[a] for a in path])])
+                hfull = o.encoder_query(htri[0], j, k_mem, v_mem)
+                z = o.head_logits(k, self.h_last, hfull)
+                lists[u] = self._select(z, self.s[k], n + 1 + k)
+                all_logits[u] = z
+            if not forced_path:
+                for v in range(t.n):
+                    if t.depth[v] == k + 1:
+                        toks[v] = int(lists[t.parent[v]][t.ranks[v][-1]])
+        return lists, all_logits
+
     def _select(self, z: np.ndarray, s: int, j: int) -> List[int]:
         f = self.forcing
         if f is None:
@@ -511,11 +558,16 @@ class Decoder:
             return [gj] + top_s(z, s - 1, exclude=gj)
         return top_s(z, s, exclude=gj)
 
-    def assemble(self, lists: Sequence[Sequence[int]]) -> List[int]:
-        """Tree tokens: root = pending; node (r_0..r_k) = lists[k][r_k]."""
+    def assemble(self, lists) -> List[int]:
+        """Tree tokens: root = pending; node (r_0..r_k) = lists[k][r_k] for
+        chain drafting, or the rank-r_k token of its parent's own list for
+        branch-conditioned drafting."""
+        t = self.tree
         toks = [self.pending]
-        for r in self.tree.ranks[1:]:
-            toks.append(int(lists[len(r) - 1][r[-1]]))
+        for u in range(1, t.n):
+            r = t.ranks[u]
+            src = lists[t.parent[u]] if self.branch else lists[len(r) - 1]
+            toks.append(int(src[r[-1]]))
         return toks
 
     # -- verify (Sec. 4.3) ------------------------------------------------
@@ -575,7 +627,12 @@ class Decoder:
         newly generated tokens (accepted draft tokens then the bonus) and
         the step's artefacts.  The overrides let a test drive the oracle
         along another run's tree tokens or accepted path."""
-        lists, dlogits = self.draft() if self.K else ([], None)
+        if not self.K:
+            lists, dlogits = [], None
+        elif self.branch:
+            lists, dlogits = self.draft_branches()
+        else:
+            lists, dlogits = self.draft()
         toks = self.assemble(lists) if tree_tokens_override is None else list(tree_tokens_override)
         logits, h, tkv = self.verify(toks)
         amax = [argmax_lowest(r) for r in logits]
