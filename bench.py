@@ -16,7 +16,9 @@ steps run first, then exactly K steps are timed; the line printed is
 Also reported: the verify GEMM kernel's achieved HBM bandwidth from HIP
 events around each of its launches in the timed steps (roofline), the whole
 verify pass's fraction of HBM peak, the plain greedy decoding rate of the
-same GPU path (tree of one node) and the CPU oracle on a bounded sample.
+same GPU path (tree of one node), the CPU oracle on a bounded sample, and
+side measurements of the trigram lookup cache, branch-conditioned drafting
+and typical decoding.
 """
 from __future__ import annotations
 
@@ -48,6 +50,7 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--no-typical", action="store_true", help="skip the typical-decoding (T = 1) measurement")
+    ap.add_argument("--no-branch", action="store_true", help="skip the branch-conditioned drafting measurement")
     ap.add_argument("--trigram-cache", type=int, default=65536,
                     help="entries of the trigram lookup cache measured after the headline passes (0: skip)")
     return ap.parse_args()
@@ -66,6 +69,14 @@ def forcing_tables(wl, prompts, ar_streams, stride):
         ref[b, n0:n0 + len(a)] = a
         ok[b] = synth.force_table(ps[b], wl.force_seed, b, stride)
     return ref, ok
+
+
+def drafted_per_level(tree):
+    """Tree nodes with children at each depth: the draft queries per sequence
+    of each level under branch-conditioned drafting."""
+    internal = {r[:-1] for r in tree}
+    K = max(len(r) for r in tree)
+    return [sum(1 for r in internal if len(r) == k) for k in range(K)]
 
 
 def cpu_baseline(wl, weights_gpu, prompt, accept_len):
@@ -241,6 +252,45 @@ def main():
                           "hit_rate": round((h1 - h0) / max(l1 - l0, 1), 4), "same_stream": same}
             log(f"[bench] trigram cache {label}: {tri[label]}")
         spec.trigram_cache(0)
+    br = None
+    if not a.no_branch and K_levels > 0:
+        # branch-conditioned drafting: every internal tree node drafts along its
+        # own path.  Forcing keeps the accepted path on the rank-0 chain, so the
+        # stream must equal the one above; the cost is the draft at more rows.
+        spec.set_drafting(True)
+        first = spec.prefill(prompts)
+        out3 = [[int(t)] for t in first]
+        for _ in range(a.warmup):
+            toks, n, _ = spec.step()
+            for b in range(len(prompts)):
+                out3[b] += [int(x) for x in toks[b, : n[b]]]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        acc4 = 0
+        for _ in range(a.steps):
+            toks, n, _ = spec.step()
+            acc4 += int(n.sum())
+            for b in range(len(prompts)):
+                out3[b] += [int(x) for x in toks[b, : n[b]]]
+        torch.cuda.synchronize()
+        dt4 = time.perf_counter() - t0
+        spec.set_graph(False)
+        spec.profile(True)
+        for _ in range(a.steps):
+            toks, n, _ = spec.step()
+            for b in range(len(prompts)):
+                out3[b] += [int(x) for x in toks[b, : n[b]]]
+        torch.cuda.synchronize()
+        pb = spec.profile_read()
+        spec.profile(False)
+        spec.set_graph(True)
+        spec.set_drafting(False)
+        same = all(out3[b] == out[b][: len(out3[b])] for b in range(len(prompts)))
+        br = {"tokens_per_s": round(acc4 / dt4, 2), "ms_per_step": round(dt4 / a.steps * 1e3, 4),
+              "draft_ms": round(pb.ms_draft / pb.steps, 4), "chain_draft_ms": round(prof.ms_draft / prof.steps, 4),
+              "queries_per_level": [len(prompts) * r for r in drafted_per_level(synth.TREES[wl.tree])],
+              "same_stream": same}
+        log(f"[bench] branch-conditioned drafting: {br}")
     value = accepted / dt
     gemm_gbs = prof.gemm_verify_bytes / (prof.ms_gemm_verify * 1e-3) / 1e9
     verify_gbs = prof.verify_bytes / (prof.ms_verify * 1e-3) / 1e9
@@ -344,6 +394,7 @@ def main():
         "lossless_vs_greedy": lossless,
         "trigram_cache": tri,
         "typical_decoding": typ,
+        "branch_drafting": br,
         "greedy_tokens_per_s": round(ar_rate, 2),
         "speedup_vs_greedy": round(value / ar_rate, 3),
         "cpu_baseline": cpu,

@@ -151,7 +151,8 @@ enum {
   CHIMERA_DBG_VERIFY_LOGITS = 0, /* float32 [batch*n_nodes][V], last step */
   CHIMERA_DBG_DRAFT_LOGITS = 1,  /* float32 [batch][K][V], last step */
   CHIMERA_DBG_TREE_TOKENS = 2,   /* int32 [batch][n_nodes], last step */
-  CHIMERA_DBG_DRAFT_LISTS = 3,   /* int32 [batch][K][8], last step's per-head lists */
+  CHIMERA_DBG_DRAFT_LISTS = 3,   /* int32 [batch][64][8], last step's top-s list of each drafted node
+                                    (chain drafting: row k = head k; branch: row u = tree node u) */
   CHIMERA_DBG_SEQ_LEN = 4,       /* int32 [batch], committed length n */
   CHIMERA_DBG_TOKENS = 5         /* int32 [batch][max_len + 8], committed tokens then pending */
 };
@@ -203,6 +204,26 @@ chimera_status chimera_set_graph(chimera_ctx* ctx, int32_t enable);
 enum { CHIMERA_DECODE_GREEDY = 0, CHIMERA_DECODE_TYPICAL = 1 };
 chimera_status chimera_set_decoding(chimera_ctx* ctx, int32_t mode, float temperature, float eps, float delta,
                                     uint64_t seed);
+
+/* Drafting (Sec. 4.1, Sec. 4.4).  CHIMERA_DRAFT_CHAIN (the default) runs the
+ * K draft levels along the rank-0 chain: head k reads the encoder output at
+ * the position the rank-0 tokens of heads 0..k-1 reach, and its top-s list
+ * fills every tree node at depth k + 1 (rank r: the list's rank-r token).
+ * CHIMERA_DRAFT_BRANCH (branch-conditioned drafting) runs level k once for
+ * every depth-k tree node that has children, along that node's own tokens:
+ * its trigram uses its path tokens, its encoder query sees the target-state
+ * entries 0..n-1, the trigram entries 0..n and its ancestors' speculative
+ * trigram entries (the tree mask of Sec. 4.3 applied to the encoder), and a
+ * child of rank r takes the rank-r token of its parent's own list.  Both are
+ * lossless under greedy verification; on a chain-shaped tree they are the
+ * same computation.  Branch-conditioned levels run B times the level's
+ * drafted nodes as GEMM rows, so the weight bytes per level stay those of
+ * the chain.  Forcing (chimera_set_forcing) biases every drafted node's
+ * list of a level alike.  CHIMERA_DBG_DRAFT_LOGITS is kept by chain
+ * drafting only.
+ * CHIMERA_EINVAL for an unknown mode.  Takes effect from the next step. */
+enum { CHIMERA_DRAFT_CHAIN = 0, CHIMERA_DRAFT_BRANCH = 1 };
+chimera_status chimera_set_drafting(chimera_ctx* ctx, int32_t mode);
 
 /* Trigram lookup cache (Sec. 4.1.1: a fixed-size dictionary of trigram
  * encoder outputs with least-recently-used replacement).  The cache holds

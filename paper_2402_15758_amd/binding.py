@@ -11,6 +11,7 @@ LIB_PATH = os.path.join(_HERE, "libchimera.so")
 
 CHIMERA_F32, CHIMERA_BF16 = 0, 1
 CHIMERA_DECODE_GREEDY, CHIMERA_DECODE_TYPICAL = 0, 1
+CHIMERA_DRAFT_CHAIN, CHIMERA_DRAFT_BRANCH = 0, 1
 DBG_VERIFY_LOGITS, DBG_DRAFT_LOGITS, DBG_TREE_TOKENS, DBG_DRAFT_LISTS, DBG_SEQ_LEN, DBG_TOKENS = range(6)
 STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "ECAPACITY", -4: "EHIP", -5: "ESTATE"}
 
@@ -66,6 +67,7 @@ _PROTOS = {
     "chimera_debug_gemm": [I32, P, P, I32, I32, I32, ctypes.POINTER(ctypes.c_float)],
     "chimera_trigram_cache_bytes": [P, I32, PI64],
     "chimera_set_decoding": [P, I32, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_uint64],
+    "chimera_set_drafting": [P, I32],
     "chimera_set_trigram_cache": [P, P, I64, I32],
     "chimera_trigram_cache_stats": [P, PI64, PI64],
 }
@@ -187,6 +189,10 @@ def chimera_profile_read(ctx: int) -> chimera_profile:
 
 def chimera_debug_gemm(dtype: int, x_ptr: int, w_ptr: int, M: int, N: int, K: int, y_ptr: int):
     _check(lib().chimera_debug_gemm(dtype, x_ptr, w_ptr, M, N, K, ctypes.cast(y_ptr, ctypes.POINTER(ctypes.c_float))))
+
+
+def chimera_set_drafting(ctx: int, mode: int):
+    _check(lib().chimera_set_drafting(ctx, mode))
 
 
 def chimera_set_decoding(ctx: int, mode: int, temperature: float = 1.0, eps: float = 0.09, delta: float = 0.3,

@@ -113,6 +113,10 @@ struct chimera_model {
   float* rsin = nullptr;
 };
 
+// Encoder memory per sequence and stream: positions 0 .. max_len + 63, then
+// (stream 1) one slot per draft-tree node for the speculative trigram entries.
+constexpr int ENC_TREE_SLOTS = 64;
+
 struct chimera_kv {
   chimera_model* m = nullptr;
   int B = 0, max_len = 0, n_pages = 0, ps = 0, max_pages = 0, cap = 0;
@@ -143,10 +147,15 @@ struct Event2 {
 struct chimera_ctx {
   chimera_model* m = nullptr;
   chimera_kv* kv = nullptr;
-  int B = 0, N = 0, K = 0, D = 0, Mv = 0, Md = 0, G = 0, nblk_enc = 0, tok_stride = 0;
+  int B = 0, N = 0, K = 0, D = 0, Mv = 0, Md = 0, Mq = 0, G = 0, nblk_enc = 0, tok_stride = 0;
   std::vector<int> parent, rank, depth, s_k;
   std::vector<unsigned long long> anc;
   TreeMeta tree, chain;
+  // drafting plan (chimera_set_drafting): chain (0) or branch-conditioned (1)
+  int branch = 0;
+  std::vector<int> lvl_R, lvl_off;  // drafted nodes per sequence and their offset in d_nodes, per level
+  int* d_nodes = nullptr;           // [64]
+  int* tok_src = nullptr;           // [64]
   // state
   int* n = nullptr;
   int* tok = nullptr;
@@ -176,7 +185,7 @@ struct chimera_ctx {
   int* amax = nullptr;
   void* hl = nullptr;      // tiled (LM head input)
   void* hl_rm = nullptr;   // row-major copy (decode state)
-  int mt_v = 0, mt_d = 0, mt_b = 0;  // 16-row tiles of the verify, draft and per-sequence buffers
+  int mt_v = 0, mt_d = 0, mt_q = 0;  // 16-row tiles of the verify, draft-row and draft-query buffers
   float* part_o = nullptr;
   float* part_ml = nullptr;
   int* v_pos = nullptr;
@@ -465,10 +474,20 @@ StepState make_state(chimera_ctx* c) {
   s.t_lse = c->t_lse;
   s.t_H = c->t_H;
   s.t_sample = c->t_sample;
+  const TreeMeta& dm = c->branch ? c->tree : c->chain;
+  s.d_nodes = c->d_nodes;
+  s.d_parent = dm.parent;
+  s.d_rank = dm.rank;
+  s.d_path = dm.path;
+  s.tok_src = c->tok_src;
+  s.tree_slot0 = kv->cap - ENC_TREE_SLOTS;
   return s;
 }
 
-// The draft: K chain steps of trigram MLP -> encoder block -> head k -> top-s.
+// The draft: K levels of trigram MLP -> encoder block -> head k -> top-s.
+// Level k runs one query per drafted node: the rank-0 chain's node k (chain
+// drafting) or every depth-k tree node with children (branch-conditioned
+// drafting).  Level 0 also commits the previous step's encoder entries.
 void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
   chimera_model* m = c->m;
   chimera_kv* kv = c->kv;
@@ -477,13 +496,15 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
   const int hdim = H * hd, B = c->batch, K = c->K;
   const Gemm g{c, st, false};
   for (int k = 0; k < K; ++k) {
-    const int Mk = k == 0 ? B * (2 * (K + 1) + 1) : B;
-    launch_draft_rows(dt, s, m->embed, k, c->tri_in, c->mt_d, c->d_pos, c->d_kvoff, c->d_qrow, st);
+    const DraftLevel lv{k, c->lvl_R[k], c->lvl_off[k]};
+    const int Q = B * lv.R;              // query rows
+    const int Mk = draft_level_rows(s, lv);  // plus the prologue rows at level 0
+    launch_draft_rows(dt, s, m->embed, lv, c->tri_in, c->mt_d, c->d_pos, c->d_kvoff, c->d_qrow, st);
     // trigram encoder (Eq. 2); with the cache, hits fill their rows and the MLP
     // launches do nothing when every row hit
     const int* tri_skip = nullptr;
     if (c->tri_on) {
-      launch_tri_lookup(s, c->tri, k, c->htri, st);
+      launch_tri_lookup(s, c->tri, lv, c->htri, st);
       tri_skip = c->tri.miss;
     }
     GemmEpi e1;
@@ -496,9 +517,9 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
     e2.out_f = c->htri;
     e2.ldo = d;
     g.run(c->tri_a, c->mt_d, Mk, m->tri_w2, d, d, e2, 0, 0, tri_skip);
-    if (c->tri_on) launch_tri_insert(s, c->tri, k, 0, 0, 0, c->htri, st);
+    if (c->tri_on) launch_tri_insert(s, c->tri, lv, 0, 0, 0, c->htri, st);
     launch_rmsnorm(dt, c->htri, nullptr, 0, m->enc.attn_norm, c->un, c->mt_d, nullptr, Mk, d, cf.rms_eps, 0,
-                   k == 0 ? c->pro_h : nullptr, B, B + B * (K + 1), st);
+                   k == 0 ? c->pro_h : nullptr, Q, Q + B * (K + 1), st);
     GemmEpi eq;
     eq.kind = EPI_QKV;
     eq.pos = c->d_pos;
@@ -522,44 +543,52 @@ void run_draft(chimera_ctx* c, const StepState& s, hipStream_t st) {
     ea.vbase = kv->enc_v;
     ea.cap = kv->cap;
     ea.n_b = c->n;
-    ea.step = k;
+    ea.level = k;
+    ea.nodes = c->d_nodes + lv.off;
+    ea.R = lv.R;
+    ea.path = s.d_path;
+    ea.tree_slot0 = s.tree_slot0;
     ea.H = H;
     ea.hd = hd;
     ea.scale = 1.0f / std::sqrt((float)hd);
     ea.part = c->enc_part;
     ea.nblk = c->nblk_enc;
     ea.out = c->attn_c;
-    ea.o_mtiles = c->mt_b;
+    ea.o_mtiles = c->mt_q;
     ea.B = B;
     launch_enc_attn(dt, ea, st);
 
     GemmEpi eo;
     eo.kind = EPI_PARTIAL;
     eo.part = c->dparts;
-    g.run(c->attn_c, c->mt_b, B, m->enc.wo, d, hdim, eo);
-    launch_rmsnorm(dt, c->htri, c->dparts, g.splits(d, hdim), m->enc.ffn_norm, c->yn, c->mt_b, nullptr, B, d,
+    g.run(c->attn_c, c->mt_q, Q, m->enc.wo, d, hdim, eo);
+    launch_rmsnorm(dt, c->htri, c->dparts, g.splits(d, hdim), m->enc.ffn_norm, c->yn, c->mt_q, nullptr, Q, d,
                    cf.rms_eps, 1, nullptr, 0, 0, st);
     GemmEpi egu;
     egu.kind = EPI_SWIGLU;
     egu.out_t = c->hc;
-    egu.o_mtiles = c->mt_b;
-    g.run(c->yn, c->mt_b, B, m->enc.wgu, 2 * F, d, egu);
+    egu.o_mtiles = c->mt_q;
+    g.run(c->yn, c->mt_q, Q, m->enc.wgu, 2 * F, d, egu);
     GemmEpi ed;
     ed.kind = EPI_PARTIAL;
     ed.part = c->dparts;
-    g.run(c->hc, c->mt_b, B, m->enc.wdown, d, F, ed);
-    launch_draft_finish(dt, s, c->htri, c->dparts, g.splits(d, F), c->zin, c->mt_b, st);
+    g.run(c->hc, c->mt_q, Q, m->enc.wdown, d, F, ed);
+    launch_draft_finish(dt, s, lv, c->htri, c->dparts, g.splits(d, F), c->zin, c->mt_q, st);
     GemmEpi ea1;
     ea1.kind = EPI_SILU;
     ea1.out_t = c->ak;
-    ea1.o_mtiles = c->mt_b;
-    g.run(c->zin, c->mt_b, B, m->head_a[k], d, 2 * d, ea1);
+    ea1.o_mtiles = c->mt_q;
+    g.run(c->zin, c->mt_q, Q, m->head_a[k], d, 2 * d, ea1);
+    // head logits: chain drafting keeps every level ([B][K][V]); branch-
+    // conditioned drafting uses the verify logits buffer as scratch
+    float* z = c->branch ? c->logits : c->dlogits + (size_t)k * V;
+    const int64_t ldz = c->branch ? V : (int64_t)K * V;
     GemmEpi et;
     et.kind = EPI_F32;
-    et.out_f = c->dlogits + (size_t)k * V;
-    et.ldo = K * V;
-    g.run(c->ak, c->mt_b, B, m->head_theta[k], V, d, et);
-    launch_topk(c->dlogits, s, k, c->topk_v, c->topk_i, st);
+    et.out_f = z;
+    et.ldo = (int)ldz;
+    g.run(c->ak, c->mt_q, Q, m->head_theta[k], V, d, et);
+    launch_topk(z, ldz, s, lv, c->topk_v, c->topk_i, st);
   }
 }
 
@@ -589,15 +618,17 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   chimera_model* m = c->m;
   const chimera_config& cf = m->cfg;
   const size_t es = m->es, d = cf.d_model, F = cf.d_ffn, V = cf.vocab, H = cf.n_heads, hd = cf.head_dim;
-  const size_t B = c->B, K = c->K, Mv = c->Mv, Md = c->Md, N = c->N;
-  const size_t Bp = (size_t)mcap(c->B);
+  const size_t B = c->B, K = c->K, Mv = c->Mv, Md = c->Md, N = c->N, Mq = c->Mq;
+  const size_t Qp = (size_t)mcap(c->Mq);
   c->mt_v = (int)(Mv / 16);
   c->mt_d = (int)(Md / 16);
-  c->mt_b = (int)(Bp / 16);
+  c->mt_q = (int)(Qp / 16);
   c->n = a.arr<int>(B);
   c->tok = a.arr<int>(B * c->tok_stride);
   c->h_last = a.take(B * d * es);
-  c->cand = a.arr<int>(B * std::max<size_t>(K, 1) * 8);
+  c->cand = a.arr<int>(B * 64 * 8);
+  c->d_nodes = a.arr<int>(64);
+  c->tok_src = a.arr<int>(64);
   c->tree_tok = a.arr<int>(Mv);
   c->inject = a.arr<int>(B * std::max<size_t>(N, 2));
   c->inject_on = a.arr<int>(1);
@@ -624,7 +655,7 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
     if (s > 1) scr = std::max(scr, (size_t)s * M * (size_t)n_full);
   };
   const int hdim = (int)(H * hd);
-  for (size_t M : {Mv, Md, Bp, (size_t)128}) {
+  for (size_t M : {Mv, Md, Qp, (size_t)128}) {
     need(M, 3 * hdim, 3 * hdim, (int)d);
     need(M, 2 * hdim, 3 * hdim, (int)d);
     need(M, 2 * (int)F, 2 * (int)F, (int)d);
@@ -659,16 +690,16 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   c->d_kvoff = a.arr<int64_t>(Md);
   c->d_qrow = a.arr<int>(Md);
   c->qc = a.take(Md * d * es);
-  c->attn_c = a.take(Bp * d * es);
-  c->yn = a.take(Bp * d * es);
-  c->hc = a.take(Bp * F * es);
-  c->zin = a.take(Bp * 2 * d * es);
-  c->ak = a.take(Bp * d * es);
+  c->attn_c = a.take(Qp * d * es);
+  c->yn = a.take(Qp * d * es);
+  c->hc = a.take(Qp * F * es);
+  c->zin = a.take(Qp * 2 * d * es);
+  c->ak = a.take(Qp * d * es);
   c->dlogits = a.arr<float>(B * std::max<size_t>(K, 1) * V);
-  c->dparts = a.arr<float>(8 * B * d);
-  c->enc_part = a.arr<float>(B * H * c->nblk_enc * (hd + 2));
-  c->topk_v = a.arr<float>(B * 32 * 8);
-  c->topk_i = a.arr<int>(B * 32 * 8);
+  c->dparts = a.arr<float>(8 * Mq * d);
+  c->enc_part = a.arr<float>(Mq * H * c->nblk_enc * (hd + 2));
+  c->topk_v = a.arr<float>(Mq * 32 * 8);
+  c->topk_i = a.arr<int>(Mq * 32 * 8);
   auto meta = [&](TreeMeta& t) {
     t.parent = a.arr<int>(64);
     t.depth = a.arr<int>(64);
@@ -701,10 +732,40 @@ void upload_meta(TreeMeta& t, const std::vector<int>& parent, const std::vector<
   HIPCK(hipMemcpy(t.path, path.data(), 64 * 64, hipMemcpyHostToDevice));
 }
 
+// Drafted nodes per level and each verify node's list: chain drafting drafts
+// chain node k at level k and takes node u's token from level depth(u) - 1;
+// branch-conditioned drafting drafts every tree node with children and takes
+// node u's token from its parent's own list.
+void set_draft_plan(chimera_ctx* c) {
+  std::vector<int> nodes, src(64, 0);
+  std::vector<char> has_child(64, 0);
+  for (int u = 1; u < c->N; ++u) has_child[c->parent[u]] = 1;
+  c->lvl_R.assign(std::max(c->K, 1), 0);
+  c->lvl_off.assign(std::max(c->K, 1), 0);
+  for (int k = 0; k < c->K; ++k) {
+    c->lvl_off[k] = (int)nodes.size();
+    if (!c->branch)
+      nodes.push_back(k);
+    else
+      for (int u = 0; u < c->N; ++u)
+        if (c->depth[u] == k && has_child[u]) nodes.push_back(u);
+    c->lvl_R[k] = (int)nodes.size() - c->lvl_off[k];
+    REQUIRE(c->lvl_R[k] >= 1 && c->B * c->lvl_R[k] <= std::max(c->Mq, 1), CHIMERA_EINVAL,
+            "draft level larger than the context was sized for");
+  }
+  for (int u = 1; u < c->N; ++u) src[u] = c->branch ? c->parent[u] : c->depth[u] - 1;
+  nodes.resize(64, 0);
+  HIPCK(hipMemcpy(c->d_nodes, nodes.data(), 64 * sizeof(int), hipMemcpyHostToDevice));
+  HIPCK(hipMemcpy(c->tok_src, src.data(), 64 * sizeof(int), hipMemcpyHostToDevice));
+}
+
 void ctx_dims(chimera_ctx* c) {
   const chimera_config& cf = c->m->cfg;
   c->Mv = mcap(std::max(c->B * c->N, 64));
-  c->Md = mcap(std::max(c->B * (2 * (c->K + 1) + 1), 128));
+  // query rows of one draft level: B (chain drafting) or B times the level's
+  // drafted nodes (branch-conditioned drafting), fewer than N per sequence
+  c->Mq = c->B * std::max(c->N - 1, 1);
+  c->Md = mcap(std::max({c->B * (2 * (c->K + 1) + 1), c->Mq, 128}));
   c->G = (c->kv->max_len + TREE_ATTN_GROUP_POSITIONS - 1) / TREE_ATTN_GROUP_POSITIONS + 1;
   c->tok_stride = c->kv->max_len + 8;
   c->nblk_enc = (2 * c->kv->cap + cf.n_draft_heads + 1 + 255) / 256;
@@ -907,7 +968,7 @@ chimera_status chimera_kv_bytes(const chimera_model* m, int32_t max_batch, int32
     kv.n_pages = n_pages;
     kv.ps = page_size;
     kv.max_pages = (max_len + 64 + page_size - 1) / page_size;
-    kv.cap = max_len + 64;
+    kv.cap = max_len + 64 + ENC_TREE_SLOTS;
     Arena a{nullptr, 0};
     carve_kv(&kv, a);
     *bytes = (int64_t)a.off + 256;
@@ -928,7 +989,7 @@ chimera_status chimera_kv_create(chimera_model* m, int32_t max_batch, int32_t ma
       kv->n_pages = n_pages;
       kv->ps = page_size;
       kv->max_pages = (max_len + 64 + page_size - 1) / page_size;
-      kv->cap = max_len + 64;
+      kv->cap = max_len + 64 + ENC_TREE_SLOTS;
       const int64_t H = m->cfg.n_heads, hd = m->cfg.head_dim;
       kv->page_stride = 2 * H * page_size * hd;
       kv->layer_stride = (int64_t)n_pages * kv->page_stride;
@@ -1030,6 +1091,7 @@ chimera_status chimera_ctx_create(chimera_model* m, chimera_kv* kv, const int32_
         ca[u] = (u == 63) ? ~0ull : ((1ull << (u + 1)) - 1ull);
       }
       upload_meta(c->chain, cp, cr, cd, ca);
+      set_draft_plan(c);
       HIPCK(hipMemcpy(c->s_k_dev, c->s_k.data(), 8 * sizeof(int), hipMemcpyHostToDevice));
       HIPCK(hipMemset(c->inject_on, 0, sizeof(int)));
       HIPCK(hipMemset(c->tri.miss, 0, sizeof(int)));
@@ -1094,7 +1156,7 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
         e2.out_f = ctx->htri + (size_t)M * d;
         e2.ldo = d;
         g.run(ctx->tri_a, ctx->mt_d, M, m->tri_w2, d, d, e2);
-        if (ctx->tri_on) launch_tri_insert(s, ctx->tri, 0, b, p0, M, ctx->htri + (size_t)M * d, st);
+        if (ctx->tri_on) launch_tri_insert(s, ctx->tri, DraftLevel{0, 1, 0}, b, p0, M, ctx->htri + (size_t)M * d, st);
         launch_rmsnorm(dt, ctx->htri, nullptr, 0, m->enc.attn_norm, ctx->un, ctx->mt_d, nullptr, 2 * M, d, cf.rms_eps,
                        0, ctx->hl_rm, 0, M, st);
         GemmEpi ekv;
@@ -1295,9 +1357,13 @@ chimera_status chimera_debug_copy(chimera_ctx* ctx, int32_t what, void* dst, int
     size_t size = 0;
     switch (what) {
       case CHIMERA_DBG_VERIFY_LOGITS: src = ctx->logits; size = B * N * V * 4; break;
-      case CHIMERA_DBG_DRAFT_LOGITS: src = ctx->dlogits; size = B * K * V * 4; break;
+      case CHIMERA_DBG_DRAFT_LOGITS:
+        REQUIRE(!ctx->branch, CHIMERA_EINVAL, "draft logits are kept by chain drafting only");
+        src = ctx->dlogits;
+        size = B * K * V * 4;
+        break;
       case CHIMERA_DBG_TREE_TOKENS: src = ctx->tree_tok; size = B * N * 4; break;
-      case CHIMERA_DBG_DRAFT_LISTS: src = ctx->cand; size = B * K * 8 * 4; break;
+      case CHIMERA_DBG_DRAFT_LISTS: src = ctx->cand; size = B * 64 * 8 * 4; break;
       case CHIMERA_DBG_SEQ_LEN: src = ctx->n; size = B * 4; break;
       case CHIMERA_DBG_TOKENS: src = ctx->tok; size = B * ctx->tok_stride * 4; break;
       default: throw Err(CHIMERA_EINVAL, "unknown debug buffer");
@@ -1398,6 +1464,23 @@ chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, i
       throw;
     }
     cleanup();
+  });
+}
+
+chimera_status chimera_set_drafting(chimera_ctx* ctx, int32_t mode) {
+  return guard([&] {
+    check_ctx(ctx);
+    REQUIRE(mode == CHIMERA_DRAFT_CHAIN || mode == CHIMERA_DRAFT_BRANCH, CHIMERA_EINVAL, "unknown drafting mode");
+    drop_graph(ctx);
+    const int old = ctx->branch;
+    ctx->branch = mode == CHIMERA_DRAFT_BRANCH;
+    try {
+      set_draft_plan(ctx);
+    } catch (...) {
+      ctx->branch = old;
+      set_draft_plan(ctx);
+      throw;
+    }
   });
 }
 

@@ -111,19 +111,28 @@ constexpr int TREE_ATTN_TAIL_ROWS = 192;
 void launch_attn_rows(const int* n_b, const int* page_table, int max_pages, int ps, int64_t page_stride, int hd,
                       int N, int B, int64_t* rowtab, hipStream_t st);
 
+// Query row r = b * R + i of draft level `level` is draft-tree node
+// nodes[i] of sequence b, at trigram position n_b + level.  Its keys, in
+// order: target-state entries 0..n-1, trigram entries 0..n (stream 1), then
+// the trigram entries of its ancestors-or-self at depths 1..level, kept in
+// stream-1 slots tree_slot0 + node.
 struct EncAttnArgs {
-  const void* q;            // [B][ldq]
+  const void* q;            // [B*R][ldq]
   int ldq;
   const void* kbase;        // encoder memory K [B][2][H][cap][hd]
   const void* vbase;
   int cap;
   const int* n_b;           // [B]
-  int step;                 // chain step k: query at trigram position n + k
+  int level;
+  const int* nodes;         // [R] drafted draft-tree nodes of this level
+  int R;
+  const uint8_t* path;      // [64][64] draft-tree node at each depth on the root->u path
+  int tree_slot0;
   int H, hd;
   float scale;
-  float* part;              // [B][H][nblk][hd + 2]
+  float* part;              // [B*R][H][nblk][hd + 2]
   int nblk;
-  void* out;                // tiled [B][H*hd] with o_mtiles tiles
+  void* out;                // tiled [B*R][H*hd] with o_mtiles tiles
   int o_mtiles;
   int B;
 };
@@ -142,7 +151,7 @@ struct StepState {
   const int* t_rank;        // [N]
   const unsigned long long* t_anc;  // [N]
   int* s_k;                 // [K] candidates per head
-  int* cand;                // [B][K][8]
+  int* cand;                // [B][64][8]: top-s list of each drafted draft-tree node
   int* tree_tok;            // [B*N]
   const int* inject;        // [B][N-1] injected tree tokens
   int* inject_on;           // [1]
@@ -169,6 +178,20 @@ struct StepState {
   const double* t_lse;      // [B*N]
   const double* t_H;        // [B*N]
   const int* t_sample;      // [B*N]
+  // drafting plan.  The draft tree is the rank-0 chain (chain drafting: node
+  // k at depth k) or the verify tree itself (branch-conditioned drafting).
+  // Level k drafts the depth-k draft-tree nodes that have children.
+  const int* d_nodes;       // [64] drafted draft-tree nodes, level by level
+  const int* d_parent;      // [64] draft-tree parent
+  const int* d_rank;        // [64] draft-tree rank
+  const uint8_t* d_path;    // [64][64] draft-tree node at each depth on the root->u path
+  const int* tok_src;       // [N] verify node -> the cand row holding its token (rank t_rank)
+  int tree_slot0;           // stream-1 slot of draft-tree node 0 in the encoder memory
+};
+// One draft level: R drafted nodes per sequence, s.d_nodes[off .. off + R).
+// Query rows r = b * R + i; at level 0 (R = 1) the prologue rows follow.
+struct DraftLevel {
+  int level, R, off;
 };
 // Per row r of logits [rows][V]: at temperature 1 / inv_T, lse = log sum_v
 // exp(z_v), H = the entropy of softmax(z), and sample = the Gumbel-max sample
@@ -179,24 +202,27 @@ void launch_typical_stats(const float* logits, int rows, int V, int N, int b0, c
                           int fixed_pos, float inv_T, unsigned long long seed, double* lse, double* H, int* sample,
                           hipStream_t st);
 void launch_argmax(const float* logits, int M, int V, int* amax, hipStream_t st);
-// scratch: [B][32][8] values and ids
-void launch_topk(const float* logits, const StepState& s, int level, float* scratch_v, int* scratch_i,
-                 hipStream_t st);
+// Per query row r of level lv: the top-s list of z = logits + r * ld into
+// cand[b][node] (forced as set up in s).  scratch: [B*R][32][8] values and ids.
+void launch_topk(const float* logits, int64_t ld, const StepState& s, const DraftLevel& lv, float* scratch_v,
+                 int* scratch_i, hipStream_t st);
 void launch_tree_setup(const StepState& s, hipStream_t st);
 void launch_accept(int dtype, const StepState& s, hipStream_t st);
 void launch_compact(int dtype, const StepState& s, void* pool, int n_layers, int64_t layer_stride, hipStream_t st);
 void launch_advance(int dtype, const StepState& s, hipStream_t st);
 
-// Draft rows of chain step `level`.  Rows [0, B) are the chain queries
-// (trigram position n + level).  At level 0 rows [B, B + B(K+1)) are the
-// previous step's committed target-state entries and rows
-// [B + B(K+1), B + 2B(K+1)) their trigram entries.  Writes the trigram
-// inputs [rows][3d], rotary positions, encoder-memory offsets and Q rows.
-void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int tri_mtiles,
-                       int* pos, int64_t* kvoff, int* qrow, hipStream_t st);
-// zin[b] (tiled) = [h_last[b]; T(x[b] + sum_s parts[s][b])]
-void launch_draft_finish(int dtype, const StepState& s, const float* x, const float* parts, int n_parts, void* zin,
-                         int z_mtiles, hipStream_t st);
+// Rows of draft level lv.  Rows [0, B R) are the queries (trigram position
+// n + level along each drafted node's path).  At level 0 rows
+// [B, B + B(K+1)) are the previous step's committed target-state entries
+// and rows [B + B(K+1), B + 2B(K+1)) their trigram entries.  Writes the
+// trigram inputs [rows][3d], rotary positions, encoder-memory offsets and Q rows.
+int draft_level_rows(const StepState& s, const DraftLevel& lv);
+void launch_draft_rows(int dtype, const StepState& s, const void* E, const DraftLevel& lv, void* tri_in,
+                       int tri_mtiles, int* pos, int64_t* kvoff, int* qrow, hipStream_t st);
+// zin[r] (tiled) = [h_last[b]; T(x[r] + sum_s parts[s][r])], r = b R + i,
+// parts [n_parts][B R][d]
+void launch_draft_finish(int dtype, const StepState& s, const DraftLevel& lv, const float* x, const float* parts,
+                         int n_parts, void* zin, int z_mtiles, hipStream_t st);
 // Prefill chunk rows: positions p0 .. p0+M-1 of sequence b; writes verify
 // descriptors (pos, kvoff through the page table, qrow), the token list,
 // trigram inputs for the same positions and the encoder descriptors of the
@@ -220,13 +246,13 @@ struct TriCache {
   int* miss = nullptr;                  // [1]: rows left for the trigram MLP (0 skips it)
   unsigned long long* stats = nullptr;  // [2]: lookups, hits
 };
-// Draft level `level`: look up the trigram rows of draft_rows (query rows and
+// Draft level lv: look up the trigram rows of draft_rows (query rows and
 // committed trigram rows), copy hits into htri rows [r][d].
-void launch_tri_lookup(const StepState& s, const TriCache& c, int level, float* htri, hipStream_t st);
+void launch_tri_lookup(const StepState& s, const TriCache& c, const DraftLevel& lv, float* htri, hipStream_t st);
 // Insert the rows the MLP computed: draft level (prefill_M = 0, rows as in
 // draft_rows, values htri[r]) or a prefill chunk of sequence b at positions
 // p0 .. p0+prefill_M-1 (values vals[i]).  Resets the miss count.
-void launch_tri_insert(const StepState& s, const TriCache& c, int level, int b, int p0, int prefill_M,
+void launch_tri_insert(const StepState& s, const TriCache& c, const DraftLevel& lv, int b, int p0, int prefill_M,
                        const float* vals, hipStream_t st);
 
 void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,

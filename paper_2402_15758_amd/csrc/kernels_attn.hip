@@ -441,9 +441,10 @@ void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
-// Draft encoder attention: one query per sequence (trigram position n+k)
-// over the target-state entries 0..n-1 and trigram entries 0..n+k.
-// grid (key blocks of 256, H, B); each wave reduces 64 keys, four at a
+// Draft encoder attention: one query per drafted node (trigram position
+// n+k) over the target-state entries 0..n-1, the trigram entries 0..n and
+// the node's ancestors-or-self at depths 1..k, in that order.
+// grid (key blocks of 256, H, B*R); each wave reduces 64 keys, four at a
 // time: lane group sub = lane >> 4 takes key 4*kg + sub and lane c =
 // lane & 15 the head-dim slice [c*HD/16, (c+1)*HD/16).
 // ---------------------------------------------------------------------------
@@ -454,23 +455,25 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
   static_assert(DS % VEC == 0 || VEC % DS == 0, "slice");
   __shared__ float wm[4], wl[4];
   __shared__ float wo[4][HD];
-  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int blk = blockIdx.x, h = blockIdx.y, row = blockIdx.z, b = row / a.R;
+  const int node = a.nodes[row % a.R];
   const int n = a.n_b[b];
-  const int nkeys = 2 * n + a.step + 1;
+  const int nkeys = 2 * n + a.level + 1;
   const int nblk_used = (nkeys + 255) / 256;
   if (blk >= nblk_used) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane >> 4, c = lane & 15;
   float q[DS];
   {
-    const T* qrow = (const T*)a.q + (int64_t)b * a.ldq + h * HD + c * DS;
+    const T* qrow = (const T*)a.q + (int64_t)row * a.ldq + h * HD + c * DS;
 #pragma unroll
     for (int e = 0; e < DS; ++e) q[e] = ET<T>::to_f(qrow[e]);
   }
   const int key0 = blk * 256 + wave * 64;
+  const uint8_t* path = a.path + node * 64;
   auto row_ptr = [&](const void* base, int k) -> const T* {
     const int stream = k < n ? 0 : 1;
-    const int pos = k < n ? k : k - n;
+    const int pos = k < n ? k : (k <= 2 * n ? k - n : a.tree_slot0 + path[k - 2 * n]);
     return (const T*)base + ((((int64_t)b * 2 + stream) * a.H + h) * a.cap + pos) * HD + c * DS;
   };
   float sc[16];
@@ -521,7 +524,7 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
   float m = -CH_INF;
   for (int w = 0; w < 4; ++w) m = fmaxf(m, wm[w]);
   float l = 0.f;
-  float* dst = a.part + (((int64_t)b * a.H + h) * a.nblk + blk) * (HD + 2);
+  float* dst = a.part + (((int64_t)row * a.H + h) * a.nblk + blk) * (HD + 2);
   for (int i = lane; i < HD; i += 64) {
     float acc = 0.f;
     for (int w = 0; w < 4; ++w) acc = acc + wo[w][i] * exp_diff(wm[w], m);
@@ -537,15 +540,15 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
 template <typename T, int HD>
 __global__ void enc_attn_combine(const EncAttnArgs a) {
   constexpr int DPL = HD / 64;
-  const int h = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
-  const int n = a.n_b[b];
-  const int nkeys = 2 * n + a.step + 1;
+  const int h = blockIdx.x, row = blockIdx.y, lane = threadIdx.x;
+  const int n = a.n_b[row / a.R];
+  const int nkeys = 2 * n + a.level + 1;
   const int used = (nkeys + 255) / 256;
   float m = -CH_INF, l = 0.f, o[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) o[e] = 0.f;
   for (int blk = 0; blk < used; ++blk) {
-    const float* src = a.part + (((int64_t)b * a.H + h) * a.nblk + blk) * (HD + 2);
+    const float* src = a.part + (((int64_t)row * a.H + h) * a.nblk + blk) * (HD + 2);
     const float mg = src[HD], lg = src[HD + 1];
     if (mg == -CH_INF) continue;
     const float mn = fmaxf(m, mg);
@@ -556,13 +559,13 @@ __global__ void enc_attn_combine(const EncAttnArgs a) {
     m = mn;
   }
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) store_tiled<T>((T*)a.out, a.o_mtiles, b, h * HD + DPL * lane + e, o[e] / l);
+  for (int e = 0; e < DPL; ++e) store_tiled<T>((T*)a.out, a.o_mtiles, row, h * HD + DPL * lane + e, o[e] / l);
 }
 
 template <typename T, int HD>
 void enc_attn_go(const EncAttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((enc_attn_partial<T, HD>), dim3(a.nblk, a.H, a.B), dim3(256), 0, st, a);
-  hipLaunchKernelGGL((enc_attn_combine<T, HD>), dim3(a.H, a.B), dim3(64), 0, st, a);
+  hipLaunchKernelGGL((enc_attn_partial<T, HD>), dim3(a.nblk, a.H, a.B * a.R), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((enc_attn_combine<T, HD>), dim3(a.H, a.B * a.R), dim3(64), 0, st, a);
 }
 
 }  // namespace

@@ -186,16 +186,17 @@ __device__ __forceinline__ int forced_ref(const StepState& s, int b, int level, 
   return g;
 }
 
-__global__ __launch_bounds__(256) void topk_partial_kernel(const float* __restrict__ logits, StepState s, int level,
-                                                           float* __restrict__ pv, int* __restrict__ pi) {
+__global__ __launch_bounds__(256) void topk_partial_kernel(const float* __restrict__ logits, int64_t ld, StepState s,
+                                                           DraftLevel dl, float* __restrict__ pv,
+                                                           int* __restrict__ pi) {
   __shared__ float shv[4];
   __shared__ int shi[4];
-  const int split = blockIdx.x, b = blockIdx.y;
-  const int K = s.K, V = s.V;
+  const int split = blockIdx.x, r = blockIdx.y, b = r / dl.R;
+  const int V = s.V, level = dl.level;
   const int S = s.s_k[level];
   bool ok;
   const int excl = forced_ref(s, b, level, V, &ok);
-  const float* z = logits + ((int64_t)b * K + level) * V;
+  const float* z = logits + (int64_t)r * ld;
   const int lo = (int)((int64_t)V * split / TOPK_SPLIT), hi = (int)((int64_t)V * (split + 1) / TOPK_SPLIT);
   float lv[SMAX];
   int li[SMAX];
@@ -225,30 +226,31 @@ __global__ __launch_bounds__(256) void topk_partial_kernel(const float* __restri
     }
   }
   int head = 0;
-  for (int r = 0; r < S; ++r) {
+  for (int q = 0; q < S; ++q) {
     float hv = -CH_INF;
     int hi_ = 0x7fffffff;
 #pragma unroll
-    for (int q = 0; q < SMAX; ++q)
-      if (q == head) {
-        hv = lv[q];
-        hi_ = li[q];
+    for (int e = 0; e < SMAX; ++e)
+      if (e == head) {
+        hv = lv[e];
+        hi_ = li[e];
       }
     float bv = hv;
     int bi = hi_;
     block_best(bv, bi, shv, shi);
     if (bi == hi_ && hi_ != 0x7fffffff) ++head;
     if (threadIdx.x == 0) {
-      pv[((int64_t)b * TOPK_SPLIT + split) * SMAX + r] = bv;
-      pi[((int64_t)b * TOPK_SPLIT + split) * SMAX + r] = bi;
+      pv[((int64_t)r * TOPK_SPLIT + split) * SMAX + q] = bv;
+      pi[((int64_t)r * TOPK_SPLIT + split) * SMAX + q] = bi;
     }
   }
 }
 
-__global__ __launch_bounds__(64) void topk_merge_kernel(StepState s, int level, const float* __restrict__ pv,
+__global__ __launch_bounds__(64) void topk_merge_kernel(StepState s, DraftLevel lv, const float* __restrict__ pv,
                                                         const int* __restrict__ pi) {
-  const int b = blockIdx.x, lane = threadIdx.x;
-  const int V = s.V, K = s.K;
+  const int row = blockIdx.x, lane = threadIdx.x;
+  const int b = row / lv.R, node = s.d_nodes[lv.off + row % lv.R];
+  const int V = s.V, level = lv.level;
   const int S = s.s_k[level];
   bool ok;
   const int g = forced_ref(s, b, level, V, &ok);
@@ -261,16 +263,15 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(StepState s, int level, 
     const int idx = lane + 64 * q;
     const int sp = idx / SMAX, r = idx % SMAX;
     const bool valid = sp < TOPK_SPLIT && r < S;
-    cv[q] = valid ? pv[((int64_t)b * TOPK_SPLIT + sp) * SMAX + r] : -CH_INF;
-    ci[q] = valid ? pi[((int64_t)b * TOPK_SPLIT + sp) * SMAX + r] : 0x7fffffff;
+    cv[q] = valid ? pv[((int64_t)row * TOPK_SPLIT + sp) * SMAX + r] : -CH_INF;
+    ci[q] = valid ? pi[((int64_t)row * TOPK_SPLIT + sp) * SMAX + r] : 0x7fffffff;
   }
-  int* out = s.cand + ((int64_t)b * K + level) * 8;
+  int* out = s.cand + ((int64_t)b * 64 + node) * 8;
   int first = 0;
   if (ok) {
     if (lane == 0) out[0] = g;
     first = 1;
   }
-  int chain = g;
   for (int r = first; r < S; ++r) {
     float bv = -CH_INF;
     int bi = 0x7fffffff;
@@ -300,9 +301,7 @@ __global__ __launch_bounds__(64) void topk_merge_kernel(StepState s, int level, 
     }
     const int id = wi < V ? wi : 0;
     if (lane == 0) out[r] = id;
-    if (r == 0) chain = id;
   }
-  if (lane == 0) s.tok[(int64_t)b * s.tok_stride + s.n[b] + 1 + level] = ok ? g : chain;
 }
 
 __global__ void tree_setup_kernel(StepState s) {
@@ -316,7 +315,7 @@ __global__ void tree_setup_kernel(StepState s) {
   else if (s.inject_on[0])
     t = s.inject[(int64_t)b * (s.N - 1) + u - 1];
   else
-    t = s.cand[((int64_t)b * s.K + dep - 1) * 8 + s.t_rank[u]];
+    t = s.cand[((int64_t)b * 64 + s.tok_src[u]) * 8 + s.t_rank[u]];
   const int row = b * s.N + u;
   s.tree_tok[row] = t;
   const int slot = n + u;
@@ -538,17 +537,31 @@ __global__ __launch_bounds__(256) void advance_kernel(StepState s) {
   }
 }
 
+// Token at position q >= 0 of sequence b along draft-tree node `node`'s
+// path: committed tokens and the pending one (q <= n) from tok, the draft
+// positions n + depth from the drafted lists of the node's ancestors.
+// node < 0: committed tokens only (prefill and the prologue rows).
+__device__ __forceinline__ int path_token(const StepState& s, int b, int node, int q) {
+  if (node < 0) return s.tok[(int64_t)b * s.tok_stride + q];
+  const int n = s.n[b];
+  if (q <= n) return s.tok[(int64_t)b * s.tok_stride + q];
+  const int a = s.d_path[node * 64 + (q - n)];
+  return s.cand[((int64_t)b * 64 + s.d_parent[a]) * 8 + s.d_rank[a]];
+}
+
 // Trigram input t = [e(pos-2); e(pos-1); e(pos)] of one row, zero vectors
 // before the sequence start, written tiled.
 template <typename T>
-__device__ __forceinline__ void trigram_row(const StepState& s, const T* E, int b, int pos, T* dst, int mtiles,
-                                            int row) {
+__device__ __forceinline__ void trigram_row(const StepState& s, const T* E, int b, int node, int pos, T* dst,
+                                            int mtiles, int row) {
   const int d = s.d;
+  int tk[3];
+#pragma unroll
+  for (int part = 0; part < 3; ++part) tk[part] = pos - 2 + part >= 0 ? path_token(s, b, node, pos - 2 + part) : -1;
   for (int i = blockIdx.y * blockDim.x + threadIdx.x; i < 3 * d; i += gridDim.y * blockDim.x) {
     const int part = i / d, col = i % d;
-    const int p = pos - 2 + part;
     T v = ET<T>::from_f(0.f);
-    if (p >= 0) v = E[(int64_t)s.tok[(int64_t)b * s.tok_stride + p] * d + col];
+    if (tk[part] >= 0) v = E[(int64_t)tk[part] * d + col];
     copy_tiled<T>(dst, mtiles, row, i, v);
   }
 }
@@ -558,40 +571,44 @@ __device__ __forceinline__ int64_t enc_off(const StepState& s, int b, int stream
 }
 
 template <typename T>
-__global__ void draft_rows_kernel(StepState s, const T* E, int level, T* tri_in, int tri_mtiles, int* pos,
+__global__ void draft_rows_kernel(StepState s, const T* E, DraftLevel lv, T* tri_in, int tri_mtiles, int* pos,
                                   int64_t* kvoff, int* qrow) {
   const int r = blockIdx.x;
-  const int B = s.B, K1 = s.K + 1;
-  int b, p, stream, q = -1;
+  const int B = s.B, K1 = s.K + 1, Q = B * lv.R;
+  int b, p, node = -1, q = -1;
+  int64_t off;
   bool valid = true, want_tri = true;
-  if (r < B) {
-    b = r;
-    p = s.n[b] + level;
-    stream = 1;
-    q = b;
-  } else if (r < B + B * K1) {
-    const int i = r - B;
+  if (r < Q) {
+    // query: the root's trigram entry lives at stream-1 position n, a deeper
+    // node's in its own slot
+    b = r / lv.R;
+    node = s.d_nodes[lv.off + r % lv.R];
+    p = s.n[b] + lv.level;
+    q = r;
+    off = enc_off(s, b, 1, lv.level == 0 ? p : s.tree_slot0 + node);
+  } else if (r < Q + B * K1) {
+    const int i = r - Q;
     b = i / K1;
     const int e = i % K1;
     valid = e < s.pro_count[b];
     p = s.pro_base[b] + e;
-    stream = 0;
+    off = enc_off(s, b, 0, p);
     want_tri = false;
   } else {
-    const int i = r - B - B * K1;
+    const int i = r - Q - B * K1;
     b = i / K1;
     const int e = i % K1;
     valid = e < s.pro_count[b];
     p = s.pro_base[b] + e;
-    stream = 1;
+    off = enc_off(s, b, 1, p);
   }
   if (threadIdx.x == 0 && blockIdx.y == 0) {
     pos[r] = valid ? p : 0;
-    kvoff[r] = valid ? enc_off(s, b, stream, p) : -1;
+    kvoff[r] = valid ? off : -1;
     qrow[r] = q;
   }
   if (want_tri && valid) {
-    trigram_row<T>(s, E, b, p, tri_in, tri_mtiles, r);
+    trigram_row<T>(s, E, b, node, p, tri_in, tri_mtiles, r);
   } else {
     for (int i = blockIdx.y * blockDim.x + threadIdx.x; i < 3 * s.d; i += gridDim.y * blockDim.x)
       copy_tiled<T>(tri_in, tri_mtiles, r, i, ET<T>::from_f(0.f));
@@ -599,15 +616,15 @@ __global__ void draft_rows_kernel(StepState s, const T* E, int level, T* tri_in,
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void draft_finish_kernel(StepState s, const float* x, const float* parts,
-                                                           int n_parts, T* zin, int z_mtiles) {
-  const int b = blockIdx.x, d = s.d;
+__global__ __launch_bounds__(256) void draft_finish_kernel(StepState s, DraftLevel lv, const float* x,
+                                                           const float* parts, int n_parts, T* zin, int z_mtiles) {
+  const int r = blockIdx.x, b = r / lv.R, d = s.d, M = s.B * lv.R;
   const T* hl = (const T*)s.h_last + (int64_t)b * d;
   for (int i = blockIdx.y * 256 + threadIdx.x; i < d; i += gridDim.y * 256) {
-    copy_tiled<T>(zin, z_mtiles, b, i, hl[i]);
-    float f = parts[(int64_t)b * d + i];
-    for (int q = 1; q < n_parts; ++q) f = f + parts[((int64_t)q * s.B + b) * d + i];
-    store_tiled<T>(zin, z_mtiles, b, d + i, x[(int64_t)b * d + i] + f);
+    copy_tiled<T>(zin, z_mtiles, r, i, hl[i]);
+    float f = parts[(int64_t)r * d + i];
+    for (int q = 1; q < n_parts; ++q) f = f + parts[((int64_t)q * M + r) * d + i];
+    store_tiled<T>(zin, z_mtiles, r, d + i, x[(int64_t)r * d + i] + f);
   }
 }
 
@@ -630,15 +647,15 @@ __global__ void prefill_rows_kernel(StepState s, const T* E, int b, int p0, int 
     enc_qrow[M + i] = -1;
     if (i == 0) pf_n[0] = p0;  // committed length seen by the chunk's attention
   }
-  trigram_row<T>(s, E, b, p, tri_in, tri_mtiles, i);
+  trigram_row<T>(s, E, b, -1, p, tri_in, tri_mtiles, i);
 }
 
 // ---------------------------------------------------------------------------
 // Trigram lookup cache
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ unsigned long long tri_key(const StepState& s, int b, int p) {
+__device__ __forceinline__ unsigned long long tri_key(const StepState& s, int b, int node, int p) {
   auto t = [&](int q) -> unsigned long long {
-    return q >= 0 ? (unsigned long long)(s.tok[(int64_t)b * s.tok_stride + q] + 1) : 0ull;
+    return q >= 0 ? (unsigned long long)(path_token(s, b, node, q) + 1) : 0ull;
   };
   return (t(p - 2) << 42) | (t(p - 1) << 21) | t(p);
 }
@@ -652,32 +669,37 @@ __device__ __forceinline__ int tri_set(unsigned long long key, int n_sets) {
 }
 
 // Row r of a draft level (the row order of draft_rows_kernel): the trigram's
-// sequence and end position, or false for rows without a trigram.
-__device__ __forceinline__ bool draft_tri_row(const StepState& s, int level, int r, int& b, int& p) {
-  const int B = s.B, K1 = s.K + 1;
-  if (r < B) {
-    b = r;
-    p = s.n[b] + level;
+// sequence, draft-tree node (-1: committed tokens) and end position, or
+// false for rows without a trigram.
+__device__ __forceinline__ bool draft_tri_row(const StepState& s, const DraftLevel& lv, int r, int& b, int& node,
+                                              int& p) {
+  const int B = s.B, K1 = s.K + 1, Q = B * lv.R;
+  if (r < Q) {
+    b = r / lv.R;
+    node = s.d_nodes[lv.off + r % lv.R];
+    p = s.n[b] + lv.level;
     return true;
   }
-  if (r < B + B * K1) return false;  // target-state entries
-  const int i = r - B - B * K1;
+  if (r < Q + B * K1) return false;  // target-state entries
+  const int i = r - Q - B * K1;
   b = i / K1;
   const int e = i % K1;
   if (e >= s.pro_count[b]) return false;
   p = s.pro_base[b] + e;
+  node = -1;
   return true;
 }
 
-__global__ __launch_bounds__(256) void tri_lookup_kernel(StepState s, TriCache c, int level, float* __restrict__ htri) {
+__global__ __launch_bounds__(256) void tri_lookup_kernel(StepState s, TriCache c, DraftLevel lv,
+                                                         float* __restrict__ htri) {
   const int r = blockIdx.x, d = s.d;
   __shared__ int way;
-  int b = 0, p = 0;
-  if (!draft_tri_row(s, level, r, b, p)) {
+  int b = 0, node = -1, p = 0;
+  if (!draft_tri_row(s, lv, r, b, node, p)) {
     if (threadIdx.x == 0) c.hit[r] = 1;
     return;
   }
-  const unsigned long long key = tri_key(s, b, p);
+  const unsigned long long key = tri_key(s, b, node, p);
   const int set = tri_set(key, c.n_sets);
   if (threadIdx.x == 0) way = -1;
   __syncthreads();
@@ -704,27 +726,28 @@ __global__ __launch_bounds__(256) void tri_lookup_kernel(StepState s, TriCache c
 
 // One workgroup per row.  Only the first missing row of a set inserts in a
 // launch (rows of one set never race); a key already present is left alone.
-__global__ __launch_bounds__(256) void tri_insert_kernel(StepState s, TriCache c, int level, int pb, int p0,
+__global__ __launch_bounds__(256) void tri_insert_kernel(StepState s, TriCache c, DraftLevel lv, int pb, int p0,
                                                          int prefill_M, const float* __restrict__ vals) {
   const int r = blockIdx.x, d = s.d;
   __shared__ int victim;
   __shared__ int present;
   if (r == 0 && threadIdx.x == 0) *c.miss = 0;  // consumed by this level's MLP launches
-  auto row_of = [&](int rr, int& b, int& p) -> bool {
+  auto row_of = [&](int rr, int& b, int& node, int& p) -> bool {
     if (prefill_M > 0) {
       b = pb;
+      node = -1;
       p = p0 + rr;
       return true;
     }
-    return draft_tri_row(s, level, rr, b, p) && c.hit[rr] == 0;
+    return draft_tri_row(s, lv, rr, b, node, p) && c.hit[rr] == 0;
   };
-  int b = 0, p = 0;
-  if (!row_of(r, b, p)) return;
-  const unsigned long long key = tri_key(s, b, p);
+  int b = 0, node = -1, p = 0;
+  if (!row_of(r, b, node, p)) return;
+  const unsigned long long key = tri_key(s, b, node, p);
   const int set = tri_set(key, c.n_sets);
   for (int r2 = 0; r2 < r; ++r2) {  // an earlier row of this launch owns the set
-    int b2, p2;
-    if (row_of(r2, b2, p2) && tri_set(tri_key(s, b2, p2), c.n_sets) == set) return;
+    int b2, n2, p2;
+    if (row_of(r2, b2, n2, p2) && tri_set(tri_key(s, b2, n2, p2), c.n_sets) == set) return;
   }
   if (threadIdx.x == 0) {
     int v = 0, hitw = -1;
@@ -805,11 +828,12 @@ void launch_argmax(const float* logits, int M, int V, int* amax, hipStream_t st)
   hipLaunchKernelGGL(argmax_kernel, dim3(M), dim3(1024), 0, st, logits, V, amax);
 }
 
-void launch_topk(const float* logits, const StepState& s, int level, float* scratch_v, int* scratch_i,
-                 hipStream_t st) {
-  hipLaunchKernelGGL(topk_partial_kernel, dim3(TOPK_SPLIT, s.B), dim3(256), 0, st, logits, s, level, scratch_v,
+void launch_topk(const float* logits, int64_t ld, const StepState& s, const DraftLevel& lv, float* scratch_v,
+                 int* scratch_i, hipStream_t st) {
+  const int Q = s.B * lv.R;
+  hipLaunchKernelGGL(topk_partial_kernel, dim3(TOPK_SPLIT, Q), dim3(256), 0, st, logits, ld, s, lv, scratch_v,
                      scratch_i);
-  hipLaunchKernelGGL(topk_merge_kernel, dim3(s.B), dim3(64), 0, st, s, level, (const float*)scratch_v,
+  hipLaunchKernelGGL(topk_merge_kernel, dim3(Q), dim3(64), 0, st, s, lv, (const float*)scratch_v,
                      (const int*)scratch_i);
 }
 
@@ -844,26 +868,30 @@ void launch_advance(int dtype, const StepState& s, hipStream_t st) {
     hipLaunchKernelGGL(advance_kernel<float>, dim3(s.B), dim3(256), 0, st, s);
 }
 
-void launch_draft_rows(int dtype, const StepState& s, const void* E, int level, void* tri_in, int tri_mtiles,
-                       int* pos, int64_t* kvoff, int* qrow, hipStream_t st) {
-  const int rows = level == 0 ? s.B * (2 * (s.K + 1) + 1) : s.B;
-  const dim3 grid(rows, (3 * s.d + 255) / 256);
+int draft_level_rows(const StepState& s, const DraftLevel& lv) {
+  return s.B * lv.R + (lv.level == 0 ? 2 * s.B * (s.K + 1) : 0);
+}
+
+void launch_draft_rows(int dtype, const StepState& s, const void* E, const DraftLevel& lv, void* tri_in,
+                       int tri_mtiles, int* pos, int64_t* kvoff, int* qrow, hipStream_t st) {
+  const dim3 grid(draft_level_rows(s, lv), (3 * s.d + 255) / 256);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(draft_rows_kernel<bf16_t>, grid, dim3(256), 0, st, s, (const bf16_t*)E, level,
+    hipLaunchKernelGGL(draft_rows_kernel<bf16_t>, grid, dim3(256), 0, st, s, (const bf16_t*)E, lv,
                        (bf16_t*)tri_in, tri_mtiles, pos, kvoff, qrow);
   else
-    hipLaunchKernelGGL(draft_rows_kernel<float>, grid, dim3(256), 0, st, s, (const float*)E, level,
+    hipLaunchKernelGGL(draft_rows_kernel<float>, grid, dim3(256), 0, st, s, (const float*)E, lv,
                        (float*)tri_in, tri_mtiles, pos, kvoff, qrow);
 }
 
-void launch_draft_finish(int dtype, const StepState& s, const float* x, const float* parts, int n_parts, void* zin,
-                         int z_mtiles, hipStream_t st) {
+void launch_draft_finish(int dtype, const StepState& s, const DraftLevel& lv, const float* x, const float* parts,
+                         int n_parts, void* zin, int z_mtiles, hipStream_t st) {
+  const dim3 grid(s.B * lv.R, (s.d + 255) / 256);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(draft_finish_kernel<bf16_t>, dim3(s.B, (s.d + 255) / 256), dim3(256), 0, st, s, x, parts,
-                       n_parts, (bf16_t*)zin, z_mtiles);
+    hipLaunchKernelGGL(draft_finish_kernel<bf16_t>, grid, dim3(256), 0, st, s, lv, x, parts, n_parts,
+                       (bf16_t*)zin, z_mtiles);
   else
-    hipLaunchKernelGGL(draft_finish_kernel<float>, dim3(s.B, (s.d + 255) / 256), dim3(256), 0, st, s, x, parts,
-                       n_parts, (float*)zin, z_mtiles);
+    hipLaunchKernelGGL(draft_finish_kernel<float>, grid, dim3(256), 0, st, s, lv, x, parts, n_parts,
+                       (float*)zin, z_mtiles);
 }
 
 void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, int p0, int M, int* tokens_out,
@@ -877,15 +905,14 @@ void launch_prefill_rows(int dtype, const StepState& s, const void* E, int b, in
                        (float*)tri_in, tri_mtiles, enc_pos, enc_kvoff, enc_qrow, pf_n);
 }
 
-void launch_tri_lookup(const StepState& s, const TriCache& c, int level, float* htri, hipStream_t st) {
-  const int rows = level == 0 ? s.B * (2 * (s.K + 1) + 1) : s.B;
-  hipLaunchKernelGGL(tri_lookup_kernel, dim3(rows), dim3(256), 0, st, s, c, level, htri);
+void launch_tri_lookup(const StepState& s, const TriCache& c, const DraftLevel& lv, float* htri, hipStream_t st) {
+  hipLaunchKernelGGL(tri_lookup_kernel, dim3(draft_level_rows(s, lv)), dim3(256), 0, st, s, c, lv, htri);
 }
 
-void launch_tri_insert(const StepState& s, const TriCache& c, int level, int b, int p0, int prefill_M,
+void launch_tri_insert(const StepState& s, const TriCache& c, const DraftLevel& lv, int b, int p0, int prefill_M,
                        const float* vals, hipStream_t st) {
-  const int rows = prefill_M > 0 ? prefill_M : (level == 0 ? s.B * (2 * (s.K + 1) + 1) : s.B);
-  hipLaunchKernelGGL(tri_insert_kernel, dim3(rows), dim3(256), 0, st, s, c, level, b, p0, prefill_M, vals);
+  const int rows = prefill_M > 0 ? prefill_M : draft_level_rows(s, lv);
+  hipLaunchKernelGGL(tri_insert_kernel, dim3(rows), dim3(256), 0, st, s, c, lv, b, p0, prefill_M, vals);
 }
 
 void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,

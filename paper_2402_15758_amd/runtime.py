@@ -134,7 +134,7 @@ class Session:
             B.DBG_VERIFY_LOGITS: ((Bn * N, V), np.float32),
             B.DBG_DRAFT_LOGITS: ((Bn, K, V), np.float32),
             B.DBG_TREE_TOKENS: ((Bn, N), np.int32),
-            B.DBG_DRAFT_LISTS: ((Bn, K, 8), np.int32),
+            B.DBG_DRAFT_LISTS: ((Bn, 64, 8), np.int32),
             B.DBG_SEQ_LEN: ((Bn,), np.int32),
             B.DBG_TOKENS: ((Bn, self.max_len + 8), np.int32),
         }
@@ -155,6 +155,10 @@ class Session:
 
     def set_graph(self, enable: bool):
         B.chimera_set_graph(self.ctx, enable)
+
+    def set_drafting(self, branch: bool):
+        """Chain drafting (branch=False) or branch-conditioned drafting."""
+        B.chimera_set_drafting(self.ctx, B.CHIMERA_DRAFT_BRANCH if branch else B.CHIMERA_DRAFT_CHAIN)
 
     def set_decoding(self, typical: bool, temperature: float = 1.0, eps: float = 0.09, delta: float = 0.3,
                      seed: int = 0):

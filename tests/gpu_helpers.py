@@ -70,7 +70,18 @@ def check_step(art, b: int, dec: oracle.Decoder, t: float, ties: TieLog, forced=
     L = int(art["n"][b])
     tree_g = art["tree"][b]
     logits_g = art["logits"][b]
-    if dec.K:
+    if dec.K and dec.branch:
+        # branch-conditioned drafting: every drafted node's list, with the
+        # oracle's paths following the GPU's tree tokens
+        tt = dec.tree
+        for v in range(1, tt.n):
+            assert int(tree_g[v]) == int(art["lists"][b, tt.parent[v], tt.ranks[v][-1]]), v
+        lists_o, dz = dec.draft_branches(tree_tokens=[int(x) for x in tree_g])
+        for k in range(dec.K):
+            ff = forced is not None and bool(forced.ok[dec.n + 1 + k])
+            for u in dec.drafted[k]:
+                compare_lists(art["lists"][b, u, : dec.s[k]], lists_o[u], dz[u], t, ties, ff)
+    elif dec.K:
         # the oracle's draft chain follows the GPU's rank-0 tokens (each checked
         # against the oracle's own list below, with the tie rule)
         lists_o, dz = dec.draft(chain_tokens=[int(art["lists"][b, k, 0]) for k in range(dec.K)])
@@ -97,12 +108,26 @@ def check_step(art, b: int, dec: oracle.Decoder, t: float, ties: TieLog, forced=
     return new_o, err
 
 
+def used_lists(lists, tree_ranks, branch: bool):
+    """The slots of a DBG_DRAFT_LISTS array [B][64][8] that a step fills:
+    per drafted row (level k for chain drafting, internal tree node for
+    branch-conditioned drafting) its first s_k entries, concatenated."""
+    t = co.Tree(tree_ranks)
+    K = t.levels if t.n > 1 else 0
+    s_k = [max(r[k] for r in tree_ranks if len(r) > k) + 1 for k in range(K)]
+    if branch:
+        rows = [(u, s_k[t.depth[u]]) for u in range(t.n) if u in t.parent]
+    else:
+        rows = [(k, s_k[k]) for k in range(K)]
+    return np.concatenate([lists[:, r, :s] for r, s in rows], axis=1)
+
+
 def chain_nodes(tree_ranks):
     """Node ids of the rank-0 chain (root, then (0,), (0, 0), ...)."""
     return [0] + [i + 1 for i, r in enumerate(tree_ranks) if all(x == 0 for x in r)]
 
 
-def forced_lossless_run(cfg, weights, wl, steps: int, extra: int = 128):
+def forced_lossless_run(cfg, weights, wl, steps: int, extra: int = 128, branch: bool = False):
     """Run the workload's forced speculative decoding for `steps` steps and
     check, per sequence, the properties that hold at any size: the stream
     equals the GPU's greedy stream token for token, and every step accepts
@@ -134,8 +159,10 @@ def forced_lossless_run(cfg, weights, wl, steps: int, extra: int = 128):
         a = streams[b][: stride - n0]
         ref[b, n0:n0 + len(a)] = a
         ok[b] = synth.force_table(ps[b], wl.force_seed, b, stride)
-    log(f"{wl.name}: {steps} forced speculative steps, tree {wl.tree}")
+    log(f"{wl.name}: {steps} forced speculative steps, tree {wl.tree}, "
+        f"{'branch-conditioned' if branch else 'chain'} drafting")
     sp = make_session(cfg, weights, tree, max_batch=B, max_len=max_len)
+    sp.set_drafting(branch)
     sp.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
     first = sp.prefill(prompts)
     out = [[int(t)] for t in first]

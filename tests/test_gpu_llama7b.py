@@ -11,6 +11,8 @@ benchmark times.
   p_b ~ U[0.4, 0.9]): the speculative stream equals the GPU's greedy stream
   token for token, and every step accepts exactly 1 + (consecutive seeded
   successes) tokens along the rank-0 chain.
+* Branch-conditioned drafting: the teacher-forced check of every drafted
+  node's list, and the lossless forced run on the benchmark workload.
 """
 import numpy as np
 import pytest
@@ -30,13 +32,21 @@ def w7b():
     return synth.make_weights(CFG, device="cuda")
 
 
-def test_llama7b_teacher_forced_vs_oracle(w7b):
-    log("llama7b: prompt 130, T64, 2 teacher-forced steps vs float32 oracle")
+@pytest.fixture(scope="module")
+def orc7b(w7b):
+    return oracle.Oracle(CFG, synth.weights_to_numpy(w7b), compute=np.float32)
+
+
+@pytest.mark.parametrize("branch", [False, True], ids=["chain", "branch"])
+def test_llama7b_teacher_forced_vs_oracle(w7b, orc7b, branch):
+    mode = "branch-conditioned" if branch else "chain"
+    log(f"llama7b: prompt 130, T64, {mode} drafting, 2 teacher-forced steps vs float32 oracle")
     prompt = synth.make_prompt(130, CFG.vocab, 41)
     sess = make_session(CFG, w7b, synth.TREE_T64, max_len=256)
+    sess.set_drafting(branch)
     first = sess.prefill([prompt])
-    orc = oracle.Oracle(CFG, synth.weights_to_numpy(w7b), compute=np.float32)
-    dec = oracle.Decoder(orc, synth.TREE_T64)
+    orc = orc7b
+    dec = oracle.Decoder(orc, synth.TREE_T64, branch=branch)
     f_o = dec.prefill(list(prompt))
     log(f"llama7b: oracle prefill done (first token gpu {int(first[0])}, oracle {f_o})")
     ties = TieLog()
@@ -86,6 +96,10 @@ def test_llama7b_p512_lossless_and_forced_acceptance(w7b):
     assert out == out_a[0][: len(out)]
     log(f"llama7b_p512: {len(out)} tokens lossless, mean accepted {len(out) / steps:.2f}")
     sp.close()
+
+
+def test_llama7b_p512_branch_drafting_lossless_and_forced_acceptance(w7b):
+    forced_lossless_run(CFG, w7b, synth.WORKLOADS["llama7b_p512"], steps=16, branch=True)
 
 
 def test_llama7b_p4096_lossless_and_forced_acceptance(w7b):

@@ -5,7 +5,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_helpers import TieLog, check_step, compare_lists, gpu_step, log, make_session, tau
+from gpu_helpers import TieLog, check_step, compare_lists, gpu_step, log, make_session, tau, used_lists
 from oracle import chimera_oracle as co
 
 pytestmark = pytest.mark.gpu
@@ -310,8 +310,9 @@ def _bits(a):
     return a.view(np.uint32) if a.dtype == np.float32 else a
 
 
-@pytest.mark.parametrize("model,entries", [("tiny", 4096), ("tiny", 8), ("small_bf16", 4096)])
-def test_trigram_cache_is_exact(model, entries):
+@pytest.mark.parametrize("model,entries,branch", [("tiny", 4096, False), ("tiny", 8, False),
+                                                 ("small_bf16", 4096, False), ("small_bf16", 4096, True)])
+def test_trigram_cache_is_exact(model, entries, branch):
     """Two passes over one prompt with and without the cache: every step's
     tokens, tree, draft lists, accepted path and verify logits are
     bit-identical.  The second pass repeats the first pass's trigrams, so
@@ -322,12 +323,14 @@ def test_trigram_cache_is_exact(model, entries):
     else:
         cfg, tree = synth.small_config(n_layers=2, d_model=512, n_heads=4, head_dim=128, d_ffn=1024, vocab=2048,
                                        n_draft_heads=4, dtype="bf16"), synth.TREE_T32
-    log(f"trigram cache: {model}, {entries} entries, 2 passes x 10 steps")
-    s_k = [max(r[k] for r in tree if len(r) > k) + 1 for k in range(max(len(r) for r in tree))]
+    log(f"trigram cache: {model}, {entries} entries, {'branch' if branch else 'chain'} drafting, "
+        "2 passes x 10 steps")
     w = synth.make_weights(cfg, device="cuda")
     prompt = synth.make_prompt(45, cfg.vocab, 11)
     plain = make_session(cfg, w, tree, max_len=256)
     cached = make_session(cfg, w, tree, max_len=256)
+    plain.set_drafting(branch)
+    cached.set_drafting(branch)
     cached.trigram_cache(entries)
     per_pass = []
     for rep in range(2):
@@ -339,9 +342,8 @@ def test_trigram_cache_is_exact(model, entries):
             a1, a2 = gpu_step(plain), gpu_step(cached)
             for key in a1:
                 x1, x2 = a1[key], a2[key]
-                if key == "lists":  # slots past a level's candidate count are unused scratch
-                    x1 = np.concatenate([x1[:, k, :s] for k, s in enumerate(s_k)], axis=1)
-                    x2 = np.concatenate([x2[:, k, :s] for k, s in enumerate(s_k)], axis=1)
+                if key == "lists":  # slots past a row's candidate count are unused scratch
+                    x1, x2 = used_lists(x1, tree, branch), used_lists(x2, tree, branch)
                 assert np.array_equal(_bits(x1), _bits(x2)), (rep, step, key)
         after = cached.trigram_stats()
         per_pass.append((after[0] - before[0], after[1] - before[1]))
@@ -432,3 +434,122 @@ def test_tiny_typical_decoding_teacher_forced(tree_name):
         lens.append(L)
     log(f"typical decoding: accepted lengths {lens}, {ties} near-ties")
     sess.close()
+
+
+# ---------------------------------------------------------------------------
+# Branch-conditioned drafting (tree reading of Sec. 4.4)
+# ---------------------------------------------------------------------------
+CHAIN3 = [(0,), (0, 0), (0, 0, 0)]
+CHAIN4 = [(0,), (0, 0), (0, 0, 0), (0, 0, 0, 0)]
+WIDE = [(0,), (1,), (2,), (0, 0), (0, 1), (1, 0), (1, 2), (2, 0), (0, 0, 0), (0, 1, 0), (1, 0, 0), (1, 2, 1)]
+
+
+@pytest.mark.parametrize("model", ["tiny", "small_bf16"])
+def test_branch_drafting_on_a_chain_tree_is_chain_drafting(tiny, small, model):
+    """On a chain-shaped tree the drafted nodes are the chain's, and the two
+    modes run the same arithmetic in the same order: bit-identical steps."""
+    if model == "tiny":
+        cfg, w, ranks = tiny[0], tiny[1], CHAIN3
+    else:
+        cfg, w, ranks = SMALL, small[0], CHAIN4
+    log(f"branch drafting: {model}, chain tree, 10 steps in both modes")
+    prompt = synth.make_prompt(40, cfg.vocab, 8)
+    a = make_session(cfg, w, ranks, max_len=256)
+    b = make_session(cfg, w, ranks, max_len=256)
+    b.set_drafting(True)
+    assert list(a.prefill([prompt])) == list(b.prefill([prompt]))
+    for step in range(10):
+        x, y = gpu_step(a), gpu_step(b)
+        for key in x:
+            u, v = x[key], y[key]
+            if key == "lists":
+                u, v = used_lists(u, ranks, False), used_lists(v, ranks, True)
+            assert np.array_equal(_bits(u), _bits(v)), (step, key)
+    a.close()
+    b.close()
+
+
+@pytest.mark.parametrize("tree_name", ["T8", "WIDE"])
+def test_tiny_branch_drafting_teacher_forced(tiny, tree_name):
+    """Every drafted node's list against the oracle's branch-conditioned
+    draft along the GPU's tree tokens, then verify and accept as for chain
+    drafting; fp32 admits no ties, and the stream is the greedy stream."""
+    cfg, w, orc, prompt = tiny
+    ranks = synth.TREE_T8 if tree_name == "T8" else WIDE
+    log(f"branch drafting: tiny fp32, {tree_name}, teacher-forced until 48 tokens")
+    sess = make_session(cfg, w, ranks, max_len=256)
+    sess.set_drafting(True)
+    first = sess.prefill([prompt])
+    dec = oracle.Decoder(orc, ranks, branch=True)
+    assert int(first[0]) == dec.prefill(list(prompt))
+    ties = TieLog()
+    out = [int(first[0])]
+    while len(out) < 48:
+        new, _ = check_step(gpu_step(sess), 0, dec, tau(cfg), ties)
+        out += new
+    assert ties.argmax_ties == 0 and ties.list_ties == 0
+    assert out[:48] == orc.greedy_ar(list(prompt), 48)
+    sess.close()
+
+
+@pytest.mark.parametrize("n0,tree", [(90, "T64"), (300, "T32")])
+def test_small_bf16_branch_drafting_teacher_forced(small, n0, tree):
+    w, orc = small
+    log(f"branch drafting: small bf16, prompt {n0}, {tree}, 8 teacher-forced steps")
+    ranks = synth.TREES[tree]
+    prompt = synth.make_prompt(n0, SMALL.vocab, 60 + n0)
+    sess = make_session(SMALL, w, ranks, max_len=1024)
+    sess.set_drafting(True)
+    first = sess.prefill([prompt])
+    dec = oracle.Decoder(orc, ranks, branch=True)
+    assert int(first[0]) == dec.prefill(list(prompt))
+    ties = TieLog()
+    for _ in range(8):
+        check_step(gpu_step(sess), 0, dec, tau(SMALL), ties)
+    log(f"ties: argmax {ties.argmax_ties}, lists {ties.list_ties}")
+
+
+def test_small_bf16_branch_drafting_batch_forced(small):
+    """Batch of 3 ragged sequences, T32, forced acceptance, graph replay:
+    each sequence is its own greedy stream, every step accepts 1 +
+    (consecutive successes), and the oracle's parity holds per sequence."""
+    import torch
+    w, orc = small
+    log("branch drafting: small bf16, batch 3 ragged, T32, forced")
+    lens = [70, 130, 200]
+    prompts = [synth.make_prompt(n, SMALL.vocab, 700 + n) for n in lens]
+    max_len, G = 512, 40
+    stride = max_len + 8
+    ar_s = make_session(SMALL, w, (), max_batch=3, max_len=max_len)
+    out_a, _ = ar_s.generate(prompts, G + 8)
+    ar_s.close()
+    ref = np.full((3, stride), -1, dtype=np.int32)
+    oks = []
+    for b, n in enumerate(lens):
+        ref[b, n:n + G + 8] = out_a[b]
+        oks.append(synth.force_table([0.5, 0.7, 0.9][b], 6, b, stride))
+    ok = np.stack(oks)
+    sp = make_session(SMALL, w, synth.TREE_T32, max_batch=3, max_len=max_len)
+    sp.set_drafting(True)
+    sp.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+    first = sp.prefill(prompts)
+    decs = []
+    for b in range(3):
+        d = oracle.Decoder(orc, synth.TREE_T32, oracle.Forcing(ref[b], ok[b]), branch=True)
+        assert d.prefill(list(prompts[b])) == int(first[b])
+        decs.append(d)
+    ties = TieLog()
+    outs = [[int(f)] for f in first]
+    for _ in range(6):
+        art = gpu_step(sp)
+        for b in range(3):
+            n = decs[b].n
+            run = 0
+            while run < 4 and ok[b, n + 1 + run]:
+                run += 1
+            assert int(art["n"][b]) == 1 + run
+            new, _ = check_step(art, b, decs[b], tau(SMALL), ties, forced=decs[b].forcing)
+            outs[b] += new
+    for b in range(3):
+        assert outs[b] == out_a[b][: len(outs[b])]
+    sp.close()
