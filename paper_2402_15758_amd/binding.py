@@ -13,6 +13,7 @@ CHIMERA_F32, CHIMERA_BF16 = 0, 1
 CHIMERA_DECODE_GREEDY, CHIMERA_DECODE_TYPICAL = 0, 1
 CHIMERA_DRAFT_CHAIN, CHIMERA_DRAFT_BRANCH = 0, 1
 DBG_VERIFY_LOGITS, DBG_DRAFT_LOGITS, DBG_TREE_TOKENS, DBG_DRAFT_LISTS, DBG_SEQ_LEN, DBG_TOKENS = range(6)
+CHIMERA_OK, CHIMERA_EINVAL, CHIMERA_ENOMEM, CHIMERA_ECAPACITY, CHIMERA_EHIP, CHIMERA_ESTATE = 0, -1, -2, -3, -4, -5
 STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "ECAPACITY", -4: "EHIP", -5: "ESTATE"}
 
 

@@ -313,7 +313,7 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
 // [0, nbig) own CBA column blocks, the others CBA - 1.
 template <typename T, int MB, int CBA>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const GemmEpi e, int kind, int nbig) {
-  constexpr int PF = MB == 1 ? 4 : 3;
+  constexpr int PF = MB == 1 ? 4 : (MB >= 8 ? 2 : 3);
   if (sh.skip && *sh.skip == 0) return;
   __shared__ f32x4 red[4 * MB * CBA * 64];
   const int kblocks = sh.K / (4 * ET<T>::VEC);
@@ -386,6 +386,18 @@ void gemm_mb(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, i
   }
 }
 
+// 128-row tiles: the LDS reduction buffer (4 MB CBA KiB) limits runs to 4 blocks.
+template <typename T>
+void gemm_mb8(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, int nbig, hipStream_t st,
+              hipEvent_t ea, hipEvent_t eb) {
+  switch (cba) {
+    case 1: gemm_launch<T, 8, 1>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 2: gemm_launch<T, 8, 2>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 3: gemm_launch<T, 8, 3>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    default: gemm_launch<T, 8, 4>(s, e, kind, nwg, nbig, st, ea, eb); break;
+  }
+}
+
 template <typename T>
 void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   const int nbc = s.nb_count ? s.nb_count : s.N / 16;
@@ -399,10 +411,16 @@ void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st, hipEvent_t ev_
   const bool finish = s.splits > 1 && e.kind != EPI_PARTIAL;
   const int kind = finish ? EPI_PARTIAL : e.kind;
   hipEvent_t eb = finish ? nullptr : ev_stop;
+  // Rows per workgroup: every output element's arithmetic is the same for
+  // any MB (the waves split the reduction, not the rows), so the choice only
+  // trades weight re-reads against activation traffic.  Above 64 rows a
+  // 128-row tile halves the weight re-reads when the buffer holds whole tiles.
   if (s.M <= 16)
     gemm_mb<T, 1>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   else if (s.M <= 32)
     gemm_mb<T, 2>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
+  else if (s.M > 64 && cba <= 4 && (s.M + 127) / 128 * 8 <= s.x_mtiles)
+    gemm_mb8<T>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   else
     gemm_mb<T, 4>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   if (finish) {
