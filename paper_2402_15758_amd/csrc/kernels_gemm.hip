@@ -31,6 +31,7 @@ namespace {
 
 constexpr int NB = 4;        // 16-column blocks per weight-layout group
 constexpr int CB_MAX = 8;    // column blocks per workgroup, upper bound
+constexpr int RED_TILES = 32;  // 16x16 output tiles per wave in one LDS reduction round (4 x 32 KiB)
 constexpr int GEMM_WGS = 256;  // one workgroup per CU per reduction slice
 // Matrices at least this wide run unsplit (their epilogue needs whole sums and
 // they fill the GPU on their own); narrower ones split the reduction until a
@@ -171,6 +172,82 @@ __device__ __forceinline__ int4 ldw(const T* p) {
 // One workgroup's run of CB column blocks starting at block cb0, rows
 // [16 mb0, 16 (mb0 + MB)), reduction slice [kbeg, kend).  red: LDS of
 // [4][MB][CB][64] f32x4.
+// Epilogue of gemm_run for column blocks [J0, J0 + JN) of the run: the waves'
+// partial sums are added in wave order through LDS, then stored.
+template <typename T, int MB, int CB, int J0, int JN>
+__device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0,
+                                              const f32x4 (&acc)[MB][CB], f32x4* red, const RowMeta* rm, int wave,
+                                              int lane) {
+  const int g = lane >> 4, c16 = lane & 15;
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int jj = 0; jj < JN; ++jj) red[((wave * MB + i) * JN + jj) * 64 + lane] = acc[i][J0 + jj];
+  __syncthreads();
+  // this wave's output tiles: items it = wave, wave + 4, ... of MB * JN
+  constexpr int ITEMS = (MB * JN + 3) / 4;
+  f32x4 vv[ITEMS], vpp[ITEMS];
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const int it = wave + 4 * k;
+    if (it < MB * JN) {  // wave-uniform
+      const int i = it / JN, j = it % JN;
+      f32x4 v = red[((0 * MB + i) * JN + j) * 64 + lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * JN + j) * 64 + lane];
+      vv[k] = v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vpp[k][r] = dpp_mov<DPP_ROR8>(v[r]);  // lane column c16 ^ 8
+    }
+  }
+  if (kind == EPI_QKV) {
+    // rotary tables for every element first, then the stores
+    float cs[ITEMS][4], sn[ITEMS][4];
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+      const int it = wave + 4 * k;
+      const int i = it / JN, j = J0 + it % JN;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        cs[k][r] = 1.f;
+        sn[k][r] = 0.f;
+        const int lr = 16 * i + 4 * g + r;
+        const int row = 16 * mb0 + lr;
+        const int q = (cb0 + j) % (e.hd / 16);
+        const bool rot = (cb0 + j) < 2 * e.H * (e.hd / 16);
+        if (it < MB * JN && row < sh.M && rot) {
+          const int64_t ti = (int64_t)rm[lr].pos * (e.hd / 2) + 8 * q + (c16 & 7);
+          cs[k][r] = e.rcos[ti];
+          sn[k][r] = e.rsin[ti];
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+      const int it = wave + 4 * k;
+      const int i = it / JN, j = J0 + it % JN;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lr = 16 * i + 4 * g + r;
+        const int row = 16 * mb0 + lr;
+        if (it < MB * JN && row < sh.M) qkv_store<T>(e, rm[lr], cb0 + j, c16, vv[k][r], vpp[k][r], cs[k][r], sn[k][r]);
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const int it = wave + 4 * k;
+    const int i = it / JN, j = J0 + it % JN;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 16 * (mb0 + i) + 4 * g + r;
+      if (it < MB * JN && row < sh.M)
+        epi_elem<T>(e, kind, sh.N, sh.M, blockIdx.z, row, cb0 + j, c16, vv[k][r], vpp[k][r]);
+    }
+  }
+}
+
 template <typename T, int MB, int CB, int PF>
 __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0, int kbeg,
                                          int kend, f32x4* red, const RowMeta* rm) {
@@ -179,7 +256,6 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
   // k-loop below is a scalar branch: an MFMA ignores EXEC, so it must never
   // sit in a lane-predicated region.
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 4, c16 = lane & 15;
   const int kblocks = sh.K / (4 * VEC);
   const T* X = (const T*)sh.X + (int64_t)lane * VEC;
   const T* Wl = (const T*)sh.W + (int64_t)lane * VEC;
@@ -240,72 +316,12 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
     }
   }
 
-#pragma unroll
-  for (int i = 0; i < MB; ++i)
-#pragma unroll
-    for (int j = 0; j < CB; ++j) red[((wave * MB + i) * CB + j) * 64 + lane] = acc[i][j];
-  __syncthreads();
-  // this wave's output tiles: items it = wave, wave + 4, ... of MB * CB
-  constexpr int ITEMS = (MB * CB + 3) / 4;
-  f32x4 vv[ITEMS], vpp[ITEMS];
-#pragma unroll
-  for (int k = 0; k < ITEMS; ++k) {
-    const int it = wave + 4 * k;
-    if (it < MB * CB) {  // wave-uniform
-      const int i = it / CB, j = it % CB;
-      f32x4 v = red[((0 * MB + i) * CB + j) * 64 + lane];
-#pragma unroll
-      for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * CB + j) * 64 + lane];
-      vv[k] = v;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) vpp[k][r] = dpp_mov<DPP_ROR8>(v[r]);  // lane column c16 ^ 8
-    }
-  }
-  if (kind == EPI_QKV) {
-    // rotary tables for every element first, then the stores
-    float cs[ITEMS][4], sn[ITEMS][4];
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-      const int it = wave + 4 * k;
-      const int i = it / CB, j = it % CB;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        cs[k][r] = 1.f;
-        sn[k][r] = 0.f;
-        const int lr = 16 * i + 4 * g + r;
-        const int row = 16 * mb0 + lr;
-        const int q = (cb0 + j) % (e.hd / 16);
-        const bool rot = (cb0 + j) < 2 * e.H * (e.hd / 16);
-        if (it < MB * CB && row < sh.M && rot) {
-          const int64_t ti = (int64_t)rm[lr].pos * (e.hd / 2) + 8 * q + (c16 & 7);
-          cs[k][r] = e.rcos[ti];
-          sn[k][r] = e.rsin[ti];
-        }
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-      const int it = wave + 4 * k;
-      const int i = it / CB, j = it % CB;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int lr = 16 * i + 4 * g + r;
-        const int row = 16 * mb0 + lr;
-        if (it < MB * CB && row < sh.M) qkv_store<T>(e, rm[lr], cb0 + j, c16, vv[k][r], vpp[k][r], cs[k][r], sn[k][r]);
-      }
-    }
-    return;
-  }
-#pragma unroll
-  for (int k = 0; k < ITEMS; ++k) {
-    const int it = wave + 4 * k;
-    const int i = it / CB, j = it % CB;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = 16 * (mb0 + i) + 4 * g + r;
-      if (it < MB * CB && row < sh.M)
-        epi_elem<T>(e, kind, sh.N, sh.M, blockIdx.z, row, cb0 + j, c16, vv[k][r], vpp[k][r]);
-    }
+  // the four waves' partial sums meet in LDS, JR column blocks at a time
+  constexpr int JR = CB < RED_TILES / MB ? CB : RED_TILES / MB;
+  gemm_epilogue<T, MB, CB, 0, JR>(sh, e, kind, cb0, mb0, acc, red, rm, wave, lane);
+  if constexpr (CB > JR) {
+    __syncthreads();  // the first round's reads of red are done
+    gemm_epilogue<T, MB, CB, JR, CB - JR>(sh, e, kind, cb0, mb0, acc, red, rm, wave, lane);
   }
 }
 
@@ -314,8 +330,9 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
 template <typename T, int MB, int CBA>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const GemmEpi e, int kind, int nbig) {
   constexpr int PF = MB == 1 ? 4 : (MB >= 8 ? 2 : 3);
+  constexpr int JR = CBA < RED_TILES / MB ? CBA : RED_TILES / MB;
   if (sh.skip && *sh.skip == 0) return;
-  __shared__ f32x4 red[4 * MB * CBA * 64];
+  __shared__ f32x4 red[4 * MB * JR * 64];
   const int kblocks = sh.K / (4 * ET<T>::VEC);
   const int kps = kblocks / sh.splits;
   const int kbeg = blockIdx.z * kps;
@@ -386,7 +403,8 @@ void gemm_mb(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, i
   }
 }
 
-// 128-row tiles: the LDS reduction buffer (4 MB CBA KiB) limits runs to 4 blocks.
+// 128-row tiles; runs of up to 6 blocks fit the registers without spills.
+constexpr int CB_MAX_MB8 = 6;
 template <typename T>
 void gemm_mb8(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, int nbig, hipStream_t st,
               hipEvent_t ea, hipEvent_t eb) {
@@ -394,7 +412,9 @@ void gemm_mb8(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int cba, 
     case 1: gemm_launch<T, 8, 1>(s, e, kind, nwg, nbig, st, ea, eb); break;
     case 2: gemm_launch<T, 8, 2>(s, e, kind, nwg, nbig, st, ea, eb); break;
     case 3: gemm_launch<T, 8, 3>(s, e, kind, nwg, nbig, st, ea, eb); break;
-    default: gemm_launch<T, 8, 4>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 4: gemm_launch<T, 8, 4>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    case 5: gemm_launch<T, 8, 5>(s, e, kind, nwg, nbig, st, ea, eb); break;
+    default: gemm_launch<T, 8, 6>(s, e, kind, nwg, nbig, st, ea, eb); break;
   }
 }
 
@@ -419,7 +439,7 @@ void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st, hipEvent_t ev_
     gemm_mb<T, 1>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   else if (s.M <= 32)
     gemm_mb<T, 2>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
-  else if (s.M > 64 && cba <= 4 && (s.M + 127) / 128 * 8 <= s.x_mtiles)
+  else if (s.M > 64 && cba <= CB_MAX_MB8 && (s.M + 127) / 128 * 8 <= s.x_mtiles)
     gemm_mb8<T>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   else
     gemm_mb<T, 4>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
