@@ -70,7 +70,9 @@ size_t esize(int dt) { return dt == CHIMERA_BF16 ? 2 : 4; }
 
 // Row capacity of a tiled GEMM-input buffer that may hold up to m rows: a
 // launch with m rows reads 16-row tiles in groups of 1, 2 or 4.
-int mcap(int m) { return m <= 16 ? 16 : (m <= 32 ? 32 : (m + 63) / 64 * 64); }
+// Rows of an activation buffer: whole tiles of the GEMM row blocks that
+// read it (16, 32, 64, then 128-row blocks).
+int mcap(int m) { return m <= 16 ? 16 : (m <= 32 ? 32 : (m <= 64 ? 64 : (m + 127) / 128 * 128)); }
 
 struct BlockW {
   float* attn_norm = nullptr;

@@ -25,7 +25,11 @@ constexpr int CHUNK = 64;   // positions per chunk
 constexpr int GROUP = TREE_ATTN_GROUP_POSITIONS / CHUNK;  // chunks per shared-pass workgroup
 constexpr int TAIL_ROWS = 2 * CHUNK;  // committed rows staged by the tail pass
 constexpr int MAX_NODES = 64;
-constexpr int TAIL_QPW = 8;  // queries (one wave each) per tail-pass workgroup
+// queries (one wave each) per tail-pass workgroup: 8 (one workgroup per CU
+// at a 64-node tree and 32 heads), or 16 when the 8-query grid would need
+// more than two rounds of workgroups (large batches of small trees)
+constexpr int TAIL_QPW = 8;
+constexpr int TAIL_QPW_WIDE = 16;
 static_assert(TAIL_ROWS + MAX_NODES == TREE_ATTN_TAIL_ROWS, "tail rows");
 
 // Page-resolved offsets of the tail pass's staged rows (positions lo .. n+N-1
@@ -220,10 +224,10 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tail pass: grid (ceil(N/QPW), H, B), QPW = TAIL_QPW waves (one workgroup
-// per CU at the 64-node tree and 32 heads); wave w reduces query
-// u = QPW * blockIdx.x + w.  The workgroup stages the committed positions
-// lo .. n-1 of the last chunks followed by every tree slot (rows 0 .. nrows-1):
+// Tail pass: grid (ceil(N/QPW), H, B), QPW waves; wave w reduces query
+// u = QPW * blockIdx.x + w, with arithmetic that does not depend on QPW.
+// The workgroup stages the committed positions lo .. n-1 of the last chunks
+// followed by every tree slot (rows 0 .. nrows-1):
 //   1. loads that need nothing: n, the staged rows' page-resolved offsets
 //      (written once per pass), the queries' MFMA fragments, tree paths and
 //      depths, the first batch of shared-pass partials;
@@ -236,9 +240,9 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 // the query or key sits in the tile, so a query's scores are the same in a
 // tree and in a single-query step.
 // ---------------------------------------------------------------------------
-template <typename T, int HD>
-__global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnArgs a) {
-  constexpr int NT = 64 * TAIL_QPW;
+template <typename T, int HD, int QPW>
+__global__ __launch_bounds__(64 * QPW) void tree_attn_tail(const TreeAttnArgs a) {
+  constexpr int NT = 64 * QPW;
   constexpr int VEC = ET<T>::VEC;
   constexpr int KB = 4 * VEC;                 // reduction indices per MFMA k-block
   constexpr int ROWS = TAIL_ROWS + MAX_NODES;  // staged rows, upper bound
@@ -250,13 +254,13 @@ __global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnAr
   float* Vl = reinterpret_cast<float*>(smem);  // [ROWS][HD]
   float* Sl = Vl + ROWS * HD;                  // [QPW][ROWS]
   __shared__ int64_t rowbase[ROWS];
-  __shared__ uint8_t spath[TAIL_QPW][64];
-  __shared__ int sdepth[TAIL_QPW];
+  __shared__ uint8_t spath[QPW][64];
+  __shared__ int sdepth[QPW];
 
   const int h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
-  const int u0 = TAIL_QPW * blockIdx.x;
+  const int u0 = QPW * blockIdx.x;
   const int u = u0 + wave;
   const bool active = u < a.N;
   // 1. loads that need nothing
@@ -264,16 +268,16 @@ __global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnAr
   int4 qf[HD / KB];  // MFMA A operand: row c16 = query u0 + c16 (zero beyond the workgroup's queries)
   {
     const int uq = u0 + c16;
-    const bool qok = c16 < TAIL_QPW && uq < a.N;
+    const bool qok = c16 < QPW && uq < a.N;
     const T* qrow = (const T*)a.q + (int64_t)(b * a.N + (qok ? uq : 0)) * a.ldq + h * HD + g * VEC;
 #pragma unroll
     for (int ks = 0; ks < HD / KB; ++ks) qf[ks] = qok ? ld16(qrow + ks * KB) : int4{0, 0, 0, 0};
   }
-  for (int i = tid; i < TAIL_QPW * 64; i += NT) {
+  for (int i = tid; i < QPW * 64; i += NT) {
     const int uu = u0 + i / 64;
     spath[i / 64][i % 64] = uu < a.N ? a.path[uu * 64 + i % 64] : 0;
   }
-  if (tid < TAIL_QPW) sdepth[tid] = (u0 + tid) < a.N ? a.depth[u0 + tid] : 0;
+  if (tid < QPW) sdepth[tid] = (u0 + tid) < a.N ? a.depth[u0 + tid] : 0;
   float bm[BATCH], bl[BATCH], bo[BATCH][DPL];
   auto load_batch = [&](int g0) {
 #pragma unroll
@@ -304,11 +308,11 @@ __global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnAr
   const T* vpool = (const T*)a.vpool;
   // every load of this phase is issued before any is used: K fragments of
   // the wave's row tiles (wave w takes tiles w and w + QPW), then V rows
-  constexpr int RT_PER_WAVE = (ROWS / 16 + TAIL_QPW - 1) / TAIL_QPW;
+  constexpr int RT_PER_WAVE = (ROWS / 16 + QPW - 1) / QPW;
   int4 kf[RT_PER_WAVE][HD / KB];
 #pragma unroll
   for (int j = 0; j < RT_PER_WAVE; ++j) {
-    const int rr = 16 * (wave + TAIL_QPW * j) + c16;  // MFMA B column: staged row
+    const int rr = 16 * (wave + QPW * j) + c16;  // MFMA B column: staged row
     const T* kr = kpool + rowbase[rr < nrows ? rr : 0] + g * VEC;
 #pragma unroll
     for (int ks = 0; ks < HD / KB; ++ks) kf[j][ks] = ld16(kr + ks * KB);
@@ -351,7 +355,7 @@ __global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnAr
   }
 #pragma unroll
   for (int j = 0; j < RT_PER_WAVE; ++j) {
-    const int rt = wave + TAIL_QPW * j;
+    const int rt = wave + QPW * j;
     if (16 * rt >= nrows) break;  // wave-uniform
     const int rr = 16 * rt + c16;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -360,7 +364,7 @@ __global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnAr
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int qi = 4 * g + r;  // output row = query
-      if (qi < TAIL_QPW && rr < nrows) Sl[qi * ROWS + rr] = acc[r];
+      if (qi < QPW && rr < nrows) Sl[qi * ROWS + rr] = acc[r];
     }
   }
 #pragma unroll
@@ -426,18 +430,27 @@ __global__ __launch_bounds__(64 * TAIL_QPW) void tree_attn_tail(const TreeAttnAr
   for (int e = 0; e < DPL; ++e) store_tiled<T>((T*)a.out, a.o_mtiles, b * a.N + u, h * HD + DPL * lane + e, o[e] / l);
 }
 
-template <typename T, int HD>
-void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((tree_attn_shared<T, HD>), dim3(a.G, a.H, a.B), dim3(256), 0, st, a);
-  const size_t smem = (size_t)(TAIL_ROWS + MAX_NODES) * (HD + TAIL_QPW) * sizeof(float);
+template <typename T, int HD, int QPW>
+void tail_go(const TreeAttnArgs& a, hipStream_t st) {
+  const size_t smem = (size_t)(TAIL_ROWS + MAX_NODES) * (HD + QPW) * sizeof(float);
   static bool attr_set = false;
   if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)tree_attn_tail<T, HD>, hipFuncAttributeMaxDynamicSharedMemorySize,
+    (void)hipFuncSetAttribute((const void*)tree_attn_tail<T, HD, QPW>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)smem);
     attr_set = true;
   }
-  hipLaunchKernelGGL((tree_attn_tail<T, HD>), dim3((a.N + TAIL_QPW - 1) / TAIL_QPW, a.H, a.B), dim3(64 * TAIL_QPW),
-                     smem, st, a);
+  hipLaunchKernelGGL((tree_attn_tail<T, HD, QPW>), dim3((a.N + QPW - 1) / QPW, a.H, a.B), dim3(64 * QPW), smem, st,
+                     a);
+}
+
+template <typename T, int HD>
+void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((tree_attn_shared<T, HD>), dim3(a.G, a.H, a.B), dim3(256), 0, st, a);
+  const int64_t wgs8 = (int64_t)((a.N + TAIL_QPW - 1) / TAIL_QPW) * a.H * a.B;
+  if (wgs8 > 512)
+    tail_go<T, HD, TAIL_QPW_WIDE>(a, st);
+  else
+    tail_go<T, HD, TAIL_QPW>(a, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -553,3 +553,41 @@ def test_small_bf16_branch_drafting_batch_forced(small):
     for b in range(3):
         assert outs[b] == out_a[b][: len(outs[b])]
     sp.close()
+
+
+# ---------------------------------------------------------------------------
+# A wide batch: 9 ragged sequences x 32 nodes at 16 heads.  The verify GEMMs
+# take 128-row tiles (the last one partly filled) and the attention tail pass
+# its 16-query workgroups; each sequence is checked against the oracle.
+# ---------------------------------------------------------------------------
+WIDE_CFG = synth.small_config(n_layers=1, d_model=2048, n_heads=16, head_dim=128, d_ffn=1024, vocab=2048,
+                              n_draft_heads=4)
+
+
+def test_wide_batch_teacher_forced():
+    w = synth.make_weights(WIDE_CFG, std=0.06, device="cpu")
+    orc = oracle.Oracle(WIDE_CFG, synth.weights_to_numpy(w))
+    lens = [40, 75, 100, 130, 161, 190, 222, 260, 300]
+    log(f"wide batch: small bf16 (16 heads), batch {len(lens)} ragged, T32, 4 teacher-forced steps")
+    prompts = [synth.make_prompt(n, WIDE_CFG.vocab, 900 + n) for n in lens]
+    sp = make_session(WIDE_CFG, w, synth.TREE_T32, max_batch=len(lens), max_len=512)
+    first = sp.prefill(prompts)
+    decs = []
+    ties = TieLog()
+    for b, p in enumerate(prompts):
+        d = oracle.Decoder(orc, synth.TREE_T32)
+        f_o = d.prefill(list(p))
+        if int(first[b]) != f_o:  # admissible only as a tie of the oracle's own logits
+            logits, _, _ = orc.causal_forward(list(p))
+            z = logits[-1]
+            assert abs(z[int(first[b])] - z[f_o]) <= 2 * tau(WIDE_CFG) * (z.max() - z.min())
+            d.pending = int(first[b])
+            d.seq[-1] = int(first[b])
+            ties.argmax_ties += 1
+        decs.append(d)
+    for _ in range(4):
+        art = gpu_step(sp)
+        for b in range(len(lens)):
+            check_step(art, b, decs[b], tau(WIDE_CFG), ties)
+    log(f"ties: argmax {ties.argmax_ties}, lists {ties.list_ties}")
+    sp.close()
