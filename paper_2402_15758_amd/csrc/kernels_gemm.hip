@@ -162,6 +162,31 @@ __device__ __forceinline__ void qkv_store(const GemmEpi& e, const RowMeta& rm, i
   }
 }
 
+// The same element's value before the store: rotated Q/K or plain V.
+__device__ __forceinline__ float qkv_value(const GemmEpi& e, int blk, int c16, float v, float vp, float c, float s) {
+  const int sec = blk / (e.H * (e.hd / 16));
+  if (sec == 2) return v;
+  return c16 < 8 ? v * c - vp * s : v * c + vp * s;
+}
+
+// 8 consecutive outputs of one row of a QKV tile as one 16-byte store: half 0
+// holds lane columns 0..7 of block blk, half 1 columns 8..15.
+template <typename T>
+__device__ __forceinline__ void qkv_store16(const GemmEpi& e, const RowMeta& rm, int blk, int half, int4 v) {
+  const int hd = e.hd;
+  const int blk_head = hd / 16;
+  const int sec_blks = e.H * blk_head;
+  const int sec = blk / sec_blks, rem = blk % sec_blks;
+  const int h = rem / blk_head, q = rem % blk_head;
+  const int dim = sec < 2 ? (half ? hd / 2 : 0) + 8 * q : 16 * q + 8 * half;
+  if (sec == 0) {
+    if (rm.qrow >= 0) *reinterpret_cast<int4*>((T*)e.qout + (int64_t)rm.qrow * e.ldq + h * hd + dim) = v;
+  } else if (rm.kvoff >= 0) {
+    T* base = (T*)(sec == 1 ? e.kbase : e.vbase);
+    *reinterpret_cast<int4*>(base + rm.kvoff + h * e.head_stride + dim) = v;
+  }
+}
+
 template <typename T>
 __device__ __forceinline__ int4 ldw(const T* p) {
   typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -176,8 +201,8 @@ __device__ __forceinline__ int4 ldw(const T* p) {
 // partial sums are added in wave order through LDS, then stored.
 template <typename T, int MB, int CB, int J0, int JN>
 __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0,
-                                              const f32x4 (&acc)[MB][CB], f32x4* red, const RowMeta* rm, int wave,
-                                              int lane) {
+                                              const f32x4 (&acc)[MB][CB], f32x4* red, const RowMeta* rm, T* stage,
+                                              int wave, int lane) {
   const int g = lane >> 4, c16 = lane & 15;
 #pragma unroll
   for (int i = 0; i < MB; ++i)
@@ -222,6 +247,28 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
         }
       }
     }
+    if constexpr (sizeof(T) == 2) {
+      // each 16x16 tile goes through the wave's LDS tile, then 32 lanes store
+      // 8 consecutive outputs of one row each
+      T* tw = stage + wave * 256;
+#pragma unroll
+      for (int k = 0; k < ITEMS; ++k) {
+        const int it = wave + 4 * k;
+        if (it >= MB * JN) break;  // wave-uniform
+        const int i = it / JN, blk = cb0 + J0 + it % JN;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          tw[(4 * g + r) * 16 + c16] = ET<T>::from_f(qkv_value(e, blk, c16, vv[k][r], vpp[k][r], cs[k][r], sn[k][r]));
+        __builtin_amdgcn_wave_barrier();
+        if (lane < 32) {
+          const int lr = 16 * i + (lane & 15);
+          const int4 v = *reinterpret_cast<const int4*>(tw + (lane & 15) * 16 + 8 * (lane >> 4));
+          if (16 * mb0 + lr < sh.M) qkv_store16<T>(e, rm[lr], blk, lane >> 4, v);
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+      return;
+    }
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
       const int it = wave + 4 * k;
@@ -234,6 +281,32 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
       }
     }
     return;
+  }
+  if constexpr (sizeof(T) == 2) {
+    if (kind == EPI_SWIGLU) {
+      // the 16 x 8 outputs of a tile (gate columns c16 < 8 times their up
+      // partners) are 16 rows of 8 consecutive tiled elements: one 16-byte
+      // store per row
+      T* tw = stage + wave * 256;
+#pragma unroll
+      for (int k = 0; k < ITEMS; ++k) {
+        const int it = wave + 4 * k;
+        if (it >= MB * JN) break;  // wave-uniform
+        const int i = it / JN, blk = cb0 + J0 + it % JN;
+        if (c16 < 8) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tw[(4 * g + r) * 8 + c16] = ET<T>::from_f(silu_f(vv[k][r]) * vpp[k][r]);
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (lane < 16) {
+          const int row = 16 * (mb0 + i) + lane;
+          const int4 v = *reinterpret_cast<const int4*>(tw + lane * 8);
+          if (row < sh.M) *reinterpret_cast<int4*>((T*)e.out_t + tiled_index<T>(e.o_mtiles, row, 8 * blk)) = v;
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+      return;
+    }
   }
 #pragma unroll
   for (int k = 0; k < ITEMS; ++k) {
@@ -250,7 +323,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
 
 template <typename T, int MB, int CB, int PF>
 __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0, int kbeg,
-                                         int kend, f32x4* red, const RowMeta* rm) {
+                                         int kend, f32x4* red, const RowMeta* rm, T* stage) {
   constexpr int VEC = ET<T>::VEC;
   // The wave index is made provably wave-uniform so that every branch of the
   // k-loop below is a scalar branch: an MFMA ignores EXEC, so it must never
@@ -318,10 +391,10 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
 
   // the four waves' partial sums meet in LDS, JR column blocks at a time
   constexpr int JR = CB < RED_TILES / MB ? CB : RED_TILES / MB;
-  gemm_epilogue<T, MB, CB, 0, JR>(sh, e, kind, cb0, mb0, acc, red, rm, wave, lane);
+  gemm_epilogue<T, MB, CB, 0, JR>(sh, e, kind, cb0, mb0, acc, red, rm, stage, wave, lane);
   if constexpr (CB > JR) {
     __syncthreads();  // the first round's reads of red are done
-    gemm_epilogue<T, MB, CB, JR, CB - JR>(sh, e, kind, cb0, mb0, acc, red, rm, wave, lane);
+    gemm_epilogue<T, MB, CB, JR, CB - JR>(sh, e, kind, cb0, mb0, acc, red, rm, stage, wave, lane);
   }
 }
 
@@ -342,6 +415,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const Gem
   // QKV epilogue targets of this workgroup's rows (visible after the k-loop's
   // barrier)
   __shared__ RowMeta rm[16 * MB];
+  __shared__ __attribute__((aligned(16))) T stage[4 * 256];  // a 16x16 output tile per wave
   if (kind == EPI_QKV && threadIdx.x < 16 * MB) {
     const int row = 16 * mb0 + threadIdx.x;
     RowMeta t{-1, 0, -1};
@@ -349,11 +423,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const Gem
     rm[threadIdx.x] = t;
   }
   if (b < nbig) {
-    gemm_run<T, MB, CBA, PF>(sh, e, kind, sh.nb_off + b * CBA, mb0, kbeg, kend, red, rm);
+    gemm_run<T, MB, CBA, PF>(sh, e, kind, sh.nb_off + b * CBA, mb0, kbeg, kend, red, rm, stage);
   } else {
     if constexpr (CBA > 1)
       gemm_run<T, MB, CBA - 1, PF>(sh, e, kind, sh.nb_off + nbig * CBA + (b - nbig) * (CBA - 1), mb0, kbeg, kend,
-                                   red, rm);
+                                   red, rm, stage);
   }
 }
 
