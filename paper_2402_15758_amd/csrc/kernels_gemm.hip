@@ -201,8 +201,8 @@ __device__ __forceinline__ int4 ldw(const T* p) {
 // partial sums are added in wave order through LDS, then stored.
 template <typename T, int MB, int CB, int J0, int JN>
 __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0,
-                                              const f32x4 (&acc)[MB][CB], f32x4* red, const RowMeta* rm, T* stage,
-                                              int wave, int lane) {
+                                              const f32x4 (&acc)[MB][CB], f32x4* red, const RowMeta* rm,
+                                              float* stage, int wave, int lane) {
   const int g = lane >> 4, c16 = lane & 15;
 #pragma unroll
   for (int i = 0; i < MB; ++i)
@@ -250,7 +250,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
     if constexpr (sizeof(T) == 2) {
       // each 16x16 tile goes through the wave's LDS tile, then 32 lanes store
       // 8 consecutive outputs of one row each
-      T* tw = stage + wave * 256;
+      T* tw = reinterpret_cast<T*>(stage + wave * 256);
 #pragma unroll
       for (int k = 0; k < ITEMS; ++k) {
         const int it = wave + 4 * k;
@@ -282,12 +282,40 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
     }
     return;
   }
+  if (kind == EPI_F32 || kind == EPI_PARTIAL) {
+    // float outputs: the tile goes through the wave's LDS tile, then each lane
+    // stores 4 consecutive columns of one row (16 rows x 64 bytes)
+    float* tw = stage + wave * 256;
+    float* base;
+    int64_t ld;
+    if (kind == EPI_F32) {
+      base = e.out_f;
+      ld = e.ldo;
+    } else {
+      base = e.part + (int64_t)blockIdx.z * sh.M * sh.N;
+      ld = sh.N;
+    }
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+      const int it = wave + 4 * k;
+      if (it >= MB * JN) break;  // wave-uniform
+      const int i = it / JN, blk = cb0 + J0 + it % JN;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) tw[(4 * g + r) * 16 + c16] = vv[k][r];
+      __builtin_amdgcn_wave_barrier();
+      const int row = 16 * (mb0 + i) + (lane >> 2);
+      const float4 v = *reinterpret_cast<const float4*>(tw + (lane >> 2) * 16 + 4 * (lane & 3));
+      if (row < sh.M) *reinterpret_cast<float4*>(base + (int64_t)row * ld + 16 * blk + 4 * (lane & 3)) = v;
+      __builtin_amdgcn_wave_barrier();
+    }
+    return;
+  }
   if constexpr (sizeof(T) == 2) {
     if (kind == EPI_SWIGLU) {
       // the 16 x 8 outputs of a tile (gate columns c16 < 8 times their up
       // partners) are 16 rows of 8 consecutive tiled elements: one 16-byte
       // store per row
-      T* tw = stage + wave * 256;
+      T* tw = reinterpret_cast<T*>(stage + wave * 256);
 #pragma unroll
       for (int k = 0; k < ITEMS; ++k) {
         const int it = wave + 4 * k;
@@ -323,7 +351,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
 
 template <typename T, int MB, int CB, int PF>
 __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0, int kbeg,
-                                         int kend, f32x4* red, const RowMeta* rm, T* stage) {
+                                         int kend, f32x4* red, const RowMeta* rm, float* stage) {
   constexpr int VEC = ET<T>::VEC;
   // The wave index is made provably wave-uniform so that every branch of the
   // k-loop below is a scalar branch: an MFMA ignores EXEC, so it must never
@@ -415,7 +443,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const Gem
   // QKV epilogue targets of this workgroup's rows (visible after the k-loop's
   // barrier)
   __shared__ RowMeta rm[16 * MB];
-  __shared__ __attribute__((aligned(16))) T stage[4 * 256];  // a 16x16 output tile per wave
+  __shared__ __attribute__((aligned(16))) float stage[4 * 256];  // a 16x16 output tile per wave
   if (kind == EPI_QKV && threadIdx.x < 16 * MB) {
     const int row = 16 * mb0 + threadIdx.x;
     RowMeta t{-1, 0, -1};
