@@ -114,14 +114,18 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   // chunk c+1 are issued before chunk c is reduced.
   constexpr int PER = CHUNK * (HD / VEC) / 256;
   int4 kreg[PER], vreg[PER];
+  // K: consecutive lanes read consecutive 16-byte parts of a row (whole
+  // rows per instruction); V: consecutive lanes read the same part of
+  // consecutive rows, the order its transposed LDS writes need
+  constexpr int PARTS = HD / VEC;
   auto load_chunk = [&](int c) {
 #pragma unroll
     for (int t = 0; t < PER; ++t) {
       const int idx = tid + 256 * t;
+      const int kk = idx / PARTS, kp = idx % PARTS;
+      kreg[t] = ld16(kpool + pbase[(c - c_begin) * CHUNK + kk] + kp * VEC);
       const int key = idx % CHUNK, part = idx / CHUNK;
-      const int64_t base = pbase[(c - c_begin) * CHUNK + key] + part * VEC;
-      kreg[t] = ld16(kpool + base);
-      vreg[t] = ld16(vpool + base);
+      vreg[t] = ld16(vpool + pbase[(c - c_begin) * CHUNK + key] + part * VEC);
     }
   };
   load_chunk(c_begin);
@@ -130,8 +134,8 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 #pragma unroll
     for (int t = 0; t < PER; ++t) {
       const int idx = tid + 256 * t;
+      st16(&Ks[(idx / PARTS) * KP + (idx % PARTS) * VEC], kreg[t]);
       const int key = idx % CHUNK, part = idx / CHUNK;
-      st16(&Ks[key * KP + part * VEC], kreg[t]);
       const T* ve = reinterpret_cast<const T*>(&vreg[t]);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) Vt[(part * VEC + e) * VP + key] = ve[e];
