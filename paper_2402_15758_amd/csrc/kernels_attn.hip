@@ -465,6 +465,12 @@ void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
 // time: lane group sub = lane >> 4 takes key 4*kg + sub and lane c =
 // lane & 15 the head-dim slice [c*HD/16, (c+1)*HD/16).
 // ---------------------------------------------------------------------------
+// DS consecutive elements of a row, loaded as one vector.
+template <typename T, int DS>
+struct alignas(DS * sizeof(T) >= 16 ? 16 : DS * sizeof(T)) Frag {
+  T v[DS];
+};
+
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
   constexpr int DS = HD / 16;            // dims per lane
@@ -487,23 +493,29 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
     for (int e = 0; e < DS; ++e) q[e] = ET<T>::to_f(qrow[e]);
   }
   const int key0 = blk * 256 + wave * 64;
-  const uint8_t* path = a.path + node * 64;
-  auto row_ptr = [&](const void* base, int k) -> const T* {
-    const int stream = k < n ? 0 : 1;
-    const int pos = k < n ? k : (k <= 2 * n ? k - n : a.tree_slot0 + path[k - 2 * n]);
-    return (const T*)base + ((((int64_t)b * 2 + stream) * a.H + h) * a.cap + pos) * HD + c * DS;
-  };
+  // the node's path (draft-tree node at each depth), one entry per lane
+  const int pth = a.path[node * 64 + lane];
+  // every K and V slice of the wave's 64 keys is requested before any is
+  // used; keys past the last one read the last key's row and are masked
+  Frag<T, DS> kf[16], vf[16];
+#pragma unroll
+  for (int kg = 0; kg < 16; ++kg) {
+    const int key = min(key0 + 4 * kg + sub, nkeys - 1);
+    const int tn = __shfl(pth, max(key - 2 * n, 0));
+    const int stream = key < n ? 0 : 1;
+    const int pos = key < n ? key : (key <= 2 * n ? key - n : a.tree_slot0 + tn);
+    const int64_t off = ((((int64_t)b * 2 + stream) * a.H + h) * a.cap + pos) * HD + c * DS;
+    kf[kg] = *reinterpret_cast<const Frag<T, DS>*>((const T*)a.kbase + off);
+    vf[kg] = *reinterpret_cast<const Frag<T, DS>*>((const T*)a.vbase + off);
+  }
   float sc[16];
   float mloc = -CH_INF;
 #pragma unroll
   for (int kg = 0; kg < 16; ++kg) {
     const int key = key0 + 4 * kg + sub;
     float d = 0.f;
-    if (key < nkeys) {
-      const T* kr = row_ptr(a.kbase, key);
 #pragma unroll
-      for (int e = 0; e < DS; ++e) d = fmaf(q[e], ET<T>::to_f(kr[e]), d);
-    }
+    for (int e = 0; e < DS; ++e) d = fmaf(q[e], ET<T>::to_f(kf[kg].v[e]), d);
     d = row16_sum(d);
     sc[kg] = key < nkeys ? d * a.scale : -CH_INF;
     mloc = fmaxf(mloc, sc[kg]);
@@ -517,11 +529,8 @@ __global__ __launch_bounds__(256) void enc_attn_partial(const EncAttnArgs a) {
     const int key = key0 + 4 * kg + sub;
     const float p = (key < nkeys && mw != -CH_INF) ? expf(sc[kg] - mw) : 0.f;
     lsum = lsum + p;
-    if (key < nkeys) {
-      const T* vr = row_ptr(a.vbase, key);
 #pragma unroll
-      for (int e = 0; e < DS; ++e) o[e] = fmaf(p, ET<T>::to_f(vr[e]), o[e]);
-    }
+    for (int e = 0; e < DS; ++e) o[e] = fmaf(p, ET<T>::to_f(vf[kg].v[e]), o[e]);
   }
   lsum = rows_sum(lsum);
 #pragma unroll
