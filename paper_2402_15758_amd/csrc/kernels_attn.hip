@@ -186,21 +186,28 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
     for (int db = 0; db < HD / 16; ++db) o[db] = o[db] * alpha;
 
     if constexpr (sizeof(T) == 2) {
+      // P enters the bf16 MFMA as two bf16 terms, P = hi + lo with
+      // hi = bf16(P) and lo = bf16(P - hi), which keeps 16 of its bits
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp) {
-        bf16_t pb[8];
+        bf16_t pb[8], pl[8];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           pb[r] = f2bf(s[2 * kp][r]);
           pb[4 + r] = f2bf(s[2 * kp + 1][r]);
+          pl[r] = f2bf(s[2 * kp][r] - bf2f(pb[r]));
+          pl[4 + r] = f2bf(s[2 * kp + 1][r] - bf2f(pb[4 + r]));
         }
         const int4 bfrag = *reinterpret_cast<const int4*>(pb);
+        const int4 lfrag = *reinterpret_cast<const int4*>(pl);
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) {
           const T* vr = &Vt[(16 * db + c16) * VP];
           const int2 lo = *reinterpret_cast<const int2*>(vr + 32 * kp + 4 * g);
           const int2 hi = *reinterpret_cast<const int2*>(vr + 32 * kp + 16 + 4 * g);
-          o[db] = mfma_kb<T>(int4{lo.x, lo.y, hi.x, hi.y}, bfrag, o[db]);
+          const int4 vf = int4{lo.x, lo.y, hi.x, hi.y};
+          o[db] = mfma_kb<T>(vf, bfrag, o[db]);
+          o[db] = mfma_kb<T>(vf, lfrag, o[db]);
         }
       }
     } else {

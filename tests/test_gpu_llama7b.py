@@ -4,7 +4,7 @@ benchmark times.
 
 * Sampled outputs the oracle can compute: teacher-forced steps after a
   130-token prompt (two shared attention chunks plus the tail), checked
-  node by node against a float32 oracle holding every 7B weight.
+  node by node against a float64 oracle holding every 7B weight.
 * Properties that hold at any size, on the benchmark workload itself
   (512-token prompt, forced acceptance p = 0.7), on the 4096-token paged
   context and on the ragged batch of 8 (prompts U[256, 2048], T32,
@@ -34,13 +34,13 @@ def w7b():
 
 @pytest.fixture(scope="module")
 def orc7b(w7b):
-    return oracle.Oracle(CFG, synth.weights_to_numpy(w7b), compute=np.float32)
+    return oracle.Oracle(CFG, synth.weights_to_numpy(w7b), compute=np.float64, cache_weights=False)
 
 
 @pytest.mark.parametrize("branch", [False, True], ids=["chain", "branch"])
 def test_llama7b_teacher_forced_vs_oracle(w7b, orc7b, branch):
     mode = "branch-conditioned" if branch else "chain"
-    log(f"llama7b: prompt 130, T64, {mode} drafting, 2 teacher-forced steps vs float32 oracle")
+    log(f"llama7b: prompt 130, T64, {mode} drafting, 2 teacher-forced steps vs float64 oracle")
     prompt = synth.make_prompt(130, CFG.vocab, 41)
     sess = make_session(CFG, w7b, synth.TREE_T64, max_len=256)
     sess.set_drafting(branch)
