@@ -510,24 +510,29 @@ __global__ __launch_bounds__(256) void compact_kernel(StepState s, T* pool, int6
   }
 }
 
+// Workgroup (b, idx) moves accepted row idx of sequence b into the encoder
+// prologue rows (and h_last for the last one); workgroup (b, 0) also commits
+// the tokens and advances n.
 template <typename T>
 __global__ __launch_bounds__(256) void advance_kernel(StepState s) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x, idx = blockIdx.y;
   const int L = s.out_len[b];
-  const int n = s.n[b];
   const int K1 = s.K + 1;
   const int d = s.d;
-  if (threadIdx.x < L) s.tok[(int64_t)b * s.tok_stride + n + 1 + threadIdx.x] = s.out_tok[b * K1 + threadIdx.x];
-  const T* hl = (const T*)s.hl;
-  T* proh = (T*)s.pro_h;
-  for (int idx = 0; idx < L; ++idx) {
+  if (idx < L) {
     const int node = s.out_nodes[b * K1 + idx];
-    const T* src = hl + (int64_t)(b * s.N + node) * d;
-    T* dst = proh + ((int64_t)b * K1 + idx) * d;
-    for (int i = threadIdx.x; i < d; i += 256) dst[i] = src[i];
-    if (idx == L - 1)
-      for (int i = threadIdx.x; i < d; i += 256) ((T*)s.h_last)[(int64_t)b * d + i] = src[i];
+    const T* src = (const T*)s.hl + (int64_t)(b * s.N + node) * d;
+    T* dst = (T*)s.pro_h + ((int64_t)b * K1 + idx) * d;
+    T* hl = idx == L - 1 ? (T*)s.h_last + (int64_t)b * d : nullptr;
+    for (int i = threadIdx.x; i < d; i += 256) {
+      const T v = src[i];
+      dst[i] = v;
+      if (hl) hl[i] = v;
+    }
   }
+  if (idx != 0) return;
+  const int n = s.n[b];
+  if (threadIdx.x < L) s.tok[(int64_t)b * s.tok_stride + n + 1 + threadIdx.x] = s.out_tok[b * K1 + threadIdx.x];
   __syncthreads();
   if (threadIdx.x == 0) {
     s.pro_base[b] = n;
@@ -863,9 +868,9 @@ void launch_compact(int dtype, const StepState& s, void* pool, int n_layers, int
 
 void launch_advance(int dtype, const StepState& s, hipStream_t st) {
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(advance_kernel<bf16_t>, dim3(s.B), dim3(256), 0, st, s);
+    hipLaunchKernelGGL(advance_kernel<bf16_t>, dim3(s.B, s.K + 1), dim3(256), 0, st, s);
   else
-    hipLaunchKernelGGL(advance_kernel<float>, dim3(s.B), dim3(256), 0, st, s);
+    hipLaunchKernelGGL(advance_kernel<float>, dim3(s.B, s.K + 1), dim3(256), 0, st, s);
 }
 
 int draft_level_rows(const StepState& s, const DraftLevel& lv) {
