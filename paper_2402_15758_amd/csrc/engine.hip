@@ -192,7 +192,7 @@ struct chimera_ctx {
   float* part_ml = nullptr;
   int* v_pos = nullptr;
   int64_t* v_kvoff = nullptr;
-  int64_t* rowtab = nullptr;  // [B][TREE_ATTN_TAIL_ROWS]: tail-pass staged rows of the current verify pass
+  int64_t* rowtab = nullptr;  // [B][TREE_ATTN_TAIL_ROWS]: window rows of the current verify pass
   // trigram lookup cache (attached by chimera_set_trigram_cache; hit/miss/stats live in this arena)
   TriCache tri;
   bool tri_on = false;

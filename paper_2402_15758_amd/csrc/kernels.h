@@ -103,11 +103,17 @@ struct TreeAttnArgs {
   const int64_t* rowtab;    // [B][TREE_ATTN_TAIL_ROWS] from launch_attn_rows
 };
 void launch_tree_attn(int dtype, const TreeAttnArgs& a, hipStream_t st);
-// Rows the tail pass stages per sequence: the committed positions of the last
-// chunks (<= 127) and the N tree slots, i.e. positions lo .. n + N - 1.
-constexpr int TREE_ATTN_TAIL_ROWS = 192;
+// Each query reduces the keys at positions P_u - W + 1 .. P_u (W = this
+// window) itself; the keys before them go through the shared MFMA pass.  W
+// exceeds the depth of every tree (at most 8 levels), so the shared keys of a
+// tree query are committed ones; a prefill chain (node j at position n + j)
+// keeps its own positions in place and may be deeper.
+constexpr int TREE_ATTN_WINDOW = 16;
+// Window row table per sequence: entry k < W is position n - W + k, entry
+// W + j the slot of tree node j.
+constexpr int TREE_ATTN_TAIL_ROWS = TREE_ATTN_WINDOW + 64;
 // rowtab[b][rr] = page-resolved element offset (head and layer excluded) of
-// position lo_b + rr, written once per verify pass for all layers.
+// window row rr, written once per verify pass for all layers.
 void launch_attn_rows(const int* n_b, const int* page_table, int max_pages, int ps, int64_t page_stride, int hd,
                       int N, int B, int64_t* rowtab, hipStream_t st);
 

@@ -4,14 +4,14 @@
 // sits at position P_u = n + depth(u); it sees cache positions 0..n-1 and
 // the tree slots of its ancestors, i.e. the logical key sequence 0..P_u in
 // which position n + e maps to the tree slot of u's depth-e ancestor.  The
-// keys are reduced in 64-position chunks aligned to position 0, in chunk
-// order, with the online softmax:
-//   * chunks 0 .. c_u - 2 (c_u = P_u / 64) hold committed keys only and are
-//     shared by every query of the tree: an MFMA pass over groups of two
-//     chunks writes one partial (m, l, O) per group;
-//   * the last two chunks c_u - 1 and c_u, which contain every tree
-//     position, are reduced per query (scores by MFMA over the staged rows,
-//     softmax and PV on the VALU in logical key order) after folding the
+// keys are reduced with the online softmax in two parts, folded in order:
+//   * positions 0 .. P_u - W (W = TREE_ATTN_WINDOW, deeper than any tree)
+//     are committed keys, shared by every query of the tree: an MFMA pass
+//     over 64-position chunks aligned to position 0, in groups of two
+//     chunks, writes one partial (m, l, O) per group, each query masking
+//     the keys past its own bound;
+//   * the window P_u - W + 1 .. P_u, which holds every tree position, is
+//     reduced per query (one wave per query and head) after folding the
 //     group partials in group order.
 // The decomposition depends on P_u alone, so a query gets bit-identical
 // results whether it is a node of a 64-node tree or the single query of a
@@ -23,30 +23,23 @@ namespace {
 
 constexpr int CHUNK = 64;   // positions per chunk
 constexpr int GROUP = TREE_ATTN_GROUP_POSITIONS / CHUNK;  // chunks per shared-pass workgroup
-constexpr int TAIL_ROWS = 2 * CHUNK;  // committed rows staged by the tail pass
+constexpr int WIN = TREE_ATTN_WINDOW;  // window positions reduced per query
 constexpr int MAX_NODES = 64;
-// queries (one wave each) per tail-pass workgroup: 8 (one workgroup per CU
-// at a 64-node tree and 32 heads), or 16 when the 8-query grid would need
-// more than two rounds of workgroups (large batches of small trees)
-constexpr int TAIL_QPW = 8;
-constexpr int TAIL_QPW_WIDE = 16;
-static_assert(TAIL_ROWS + MAX_NODES == TREE_ATTN_TAIL_ROWS, "tail rows");
+static_assert(WIN + MAX_NODES == TREE_ATTN_TAIL_ROWS, "window rows");
+static_assert(WIN == 16, "the window pass maps four lanes to each window key");
 
-// Page-resolved offsets of the tail pass's staged rows (positions lo .. n+N-1
-// with lo = 64 * max(n / 64 - 1, 0)); entries past them are zero.
+// Page-resolved offsets of the window rows: entry k < WIN is position
+// n - WIN + k (committed), entry WIN + j the slot of tree node j (position
+// n + j); entries before position 0 or past the tree are zero.
 __global__ void attn_rows_kernel(const int* __restrict__ n_b, const int* __restrict__ page_table, int max_pages,
                                  int ps, int64_t page_stride, int hd, int N, int64_t* __restrict__ rowtab) {
   const int b = blockIdx.x;
   const int n = n_b[b];
-  const int cmin = n / CHUNK;
-  const int lo = (cmin >= 1 ? cmin - 1 : 0) * CHUNK;
-  const int nrows = n - lo + N;
   for (int rr = threadIdx.x; rr < TREE_ATTN_TAIL_ROWS; rr += blockDim.x) {
+    const int p = rr < WIN ? n - WIN + rr : n + rr - WIN;
     int64_t off = 0;
-    if (rr < nrows) {
-      const int p = lo + rr;
+    if (p >= 0 && (rr < WIN || rr - WIN < N))
       off = (int64_t)page_table[(int64_t)b * max_pages + p / ps] * page_stride + (int64_t)(p % ps) * hd;
-    }
     rowtab[(int64_t)b * TREE_ATTN_TAIL_ROWS + rr] = off;
   }
 }
@@ -91,11 +84,13 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
     const int pi = (c_begin * CHUNK + i) / a.ps;
     pg[t] = (i < GROUP * CHUNK && pi < a.max_pages) ? a.page_table[(int64_t)b * a.max_pages + pi] : 0;
   }
-  const int cmax = (n + a.D) / CHUNK;
-  const int last = cmax - 2;            // last chunk any query treats as shared
-  if (c_begin > last) return;
-  const int c_end = min(c_begin + GROUP - 1, last);
-  const int lim_u = (n + dep_u) / CHUNK - 2;
+  const int maxk = n + a.D - WIN;        // last position any query treats as shared
+  if (maxk < 0 || c_begin > maxk / CHUNK) return;
+  const int c_end = min(c_begin + GROUP - 1, maxk / CHUNK);
+  const int lim_u = n + dep_u - WIN;    // query u's last shared position
+  // rows past the ones written so far (positions >= n + N) may hold
+  // anything: they are staged as zeros, so masked keys add exact zeros
+  const int wlim = n + a.N;
 #pragma unroll
   for (int t = 0; t < PB; ++t) {
     const int i = tid + 256 * t;
@@ -134,9 +129,11 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 #pragma unroll
     for (int t = 0; t < PER; ++t) {
       const int idx = tid + 256 * t;
-      st16(&Ks[(idx / PARTS) * KP + (idx % PARTS) * VEC], kreg[t]);
+      const int4 zero = int4{0, 0, 0, 0};
+      st16(&Ks[(idx / PARTS) * KP + (idx % PARTS) * VEC], c * CHUNK + idx / PARTS < wlim ? kreg[t] : zero);
       const int key = idx % CHUNK, part = idx / CHUNK;
-      const T* ve = reinterpret_cast<const T*>(&vreg[t]);
+      const int4 vk = c * CHUNK + key < wlim ? vreg[t] : zero;
+      const T* ve = reinterpret_cast<const T*>(&vk);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) Vt[(part * VEC + e) * VP + key] = ve[e];
     }
@@ -152,12 +149,12 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
       for (int ks = 0; ks < HD / KB; ++ks)
         s[kb] = mfma_kb<T>(ld16(&Ks[(16 * kb + c16) * KP + ks * KB + g * VEC]), qf[ks], s[kb]);
     }
-    const bool act = valid_u && c <= lim_u;
     float mc = -CH_INF;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
+        const bool act = valid_u && c * CHUNK + 16 * kb + 4 * g + r <= lim_u;  // S^T row = key
         const float v = act ? s[kb][r] * a.scale : -CH_INF;
         s[kb][r] = v;
         mc = fmaxf(mc, v);
@@ -186,19 +183,23 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
     for (int db = 0; db < HD / 16; ++db) o[db] = o[db] * alpha;
 
     if constexpr (sizeof(T) == 2) {
-      // P enters the bf16 MFMA as two bf16 terms, P = hi + lo with
-      // hi = bf16(P) and lo = bf16(P - hi), which keeps 16 of its bits
+      // P enters the bf16 MFMA as three bf16 terms, P = hi + mid + lo with
+      // hi = bf16(P), mid = bf16(P - hi), lo = bf16(P - hi - mid): all 24
+      // bits of the float P, so every product with a bf16 V is exact and PV
+      // is as precise as a float dot product
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp) {
-        bf16_t pb[8], pl[8];
+        bf16_t ph[8], pm[8], pl[8];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          pb[r] = f2bf(s[2 * kp][r]);
-          pb[4 + r] = f2bf(s[2 * kp + 1][r]);
-          pl[r] = f2bf(s[2 * kp][r] - bf2f(pb[r]));
-          pl[4 + r] = f2bf(s[2 * kp + 1][r] - bf2f(pb[4 + r]));
+        for (int r = 0; r < 8; ++r) {
+          const float pv = s[2 * kp + r / 4][r % 4];
+          ph[r] = f2bf(pv);
+          const float r1 = pv - bf2f(ph[r]);
+          pm[r] = f2bf(r1);
+          pl[r] = f2bf(r1 - bf2f(pm[r]));
         }
-        const int4 bfrag = *reinterpret_cast<const int4*>(pb);
+        const int4 hfrag = *reinterpret_cast<const int4*>(ph);
+        const int4 mfrag = *reinterpret_cast<const int4*>(pm);
         const int4 lfrag = *reinterpret_cast<const int4*>(pl);
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) {
@@ -206,7 +207,8 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
           const int2 lo = *reinterpret_cast<const int2*>(vr + 32 * kp + 4 * g);
           const int2 hi = *reinterpret_cast<const int2*>(vr + 32 * kp + 16 + 4 * g);
           const int4 vf = int4{lo.x, lo.y, hi.x, hi.y};
-          o[db] = mfma_kb<T>(vf, bfrag, o[db]);
+          o[db] = mfma_kb<T>(vf, hfrag, o[db]);
+          o[db] = mfma_kb<T>(vf, mfrag, o[db]);
           o[db] = mfma_kb<T>(vf, lfrag, o[db]);
         }
       }
@@ -235,69 +237,54 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tail pass: grid (ceil(N/QPW), H, B), QPW waves; wave w reduces query
-// u = QPW * blockIdx.x + w, with arithmetic that does not depend on QPW.
-// The workgroup stages the committed positions lo .. n-1 of the last chunks
-// followed by every tree slot (rows 0 .. nrows-1):
-//   1. loads that need nothing: n, the staged rows' page-resolved offsets
-//      (written once per pass), the queries' MFMA fragments, tree paths and
-//      depths, the first batch of shared-pass partials;
-//   2. K fragments and V rows are requested; while they are in flight each
-//      wave folds its query's partials in group order; then S = Q K^T over
-//      every staged row by MFMA -> LDS, and V -> LDS as float;
-//   3. per query: the last two chunks in logical-position order (lane = key);
-//      PV on the VALU.
-// Each score is one MFMA dot product whose value does not depend on where
-// the query or key sits in the tile, so a query's scores are the same in a
-// tree and in a single-query step.
+// Window pass: grid (ceil(H / 4), N, B), one wave per (query u, head h):
+//   1. loads that need nothing: n, u's depth and path, the window rows'
+//      page-resolved offsets (written once per pass), the query, the first
+//      batch of group partials;
+//   2. the window's K and V rows are requested (for the scores lane
+//      4 k + j holds dims [j HD/4, (j+1) HD/4) of window key k; for PV each
+//      lane reads its own output dims of every row); while they are in
+//      flight the group partials are folded in group order;
+//   3. scores, the window's softmax step and PV in window order.
+// Window key k is position P_u - W + 1 + k: a committed row below n, the
+// slot of u's ancestor at depth p - n from n on.  Keys before position 0
+// read u's own slot and add exact zeros.
 // ---------------------------------------------------------------------------
-template <typename T, int HD, int QPW>
-__global__ __launch_bounds__(64 * QPW) void tree_attn_tail(const TreeAttnArgs a) {
-  constexpr int NT = 64 * QPW;
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
   constexpr int VEC = ET<T>::VEC;
-  constexpr int KB = 4 * VEC;                 // reduction indices per MFMA k-block
-  constexpr int ROWS = TAIL_ROWS + MAX_NODES;  // staged rows, upper bound
-  constexpr int DPL = HD / 64;                 // output dims per lane
-  constexpr int PARTS = HD / VEC;
-  constexpr int BATCH = 8;                     // shared-pass partials loaded per round trip
-  constexpr int PV_BATCH = 16;                 // keys whose V rows are read per round
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  float* Vl = reinterpret_cast<float*>(smem);  // [ROWS][HD]
-  float* Sl = Vl + ROWS * HD;                  // [QPW][ROWS]
-  __shared__ int64_t rowbase[ROWS];
-  __shared__ uint8_t spath[QPW][64];
-  __shared__ int sdepth[QPW];
-
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = lane >> 4, c16 = lane & 15;
-  const int u0 = QPW * blockIdx.x;
-  const int u = u0 + wave;
-  const bool active = u < a.N;
+  constexpr int DPL = HD / 64;   // output dims per lane
+  constexpr int LPK = 64 / WIN;  // lanes per window key
+  constexpr int DPK = HD / LPK;  // score dims per lane
+  constexpr int NQ = DPK / VEC;  // 16-byte loads per lane and row
+  constexpr int BATCH = 8;       // group partials loaded per round trip
+  static_assert(NQ >= 1 && DPK % VEC == 0, "window layout");
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int h = 4 * blockIdx.x + wave, u = blockIdx.y, b = blockIdx.z;
+  if (h >= a.H) return;  // wave-uniform
+  const int kw = lane / LPK, sub = lane % LPK;
   // 1. loads that need nothing
   const int n = a.n_b[b];
-  int4 qf[HD / KB];  // MFMA A operand: row c16 = query u0 + c16 (zero beyond the workgroup's queries)
+  const int dep = a.depth[u];
+  const int pth = a.path[u * 64 + lane];  // node at depth `lane` on u's path
+  const int64_t* rt = a.rowtab + (int64_t)b * TREE_ATTN_TAIL_ROWS;
+  const long long r_lo = rt[lane];                           // entries 0 .. 63
+  const long long r_hi = rt[64 + (lane & (TREE_ATTN_TAIL_ROWS - 64 - 1))];  // entries 64 ..
+  int4 qv[NQ];
   {
-    const int uq = u0 + c16;
-    const bool qok = c16 < QPW && uq < a.N;
-    const T* qrow = (const T*)a.q + (int64_t)(b * a.N + (qok ? uq : 0)) * a.ldq + h * HD + g * VEC;
+    const T* qrow = (const T*)a.q + (int64_t)(b * a.N + u) * a.ldq + h * HD + sub * DPK;
 #pragma unroll
-    for (int ks = 0; ks < HD / KB; ++ks) qf[ks] = qok ? ld16(qrow + ks * KB) : int4{0, 0, 0, 0};
+    for (int i = 0; i < NQ; ++i) qv[i] = ld16(qrow + i * VEC);
   }
-  for (int i = tid; i < QPW * 64; i += NT) {
-    const int uu = u0 + i / 64;
-    spath[i / 64][i % 64] = uu < a.N ? a.path[uu * 64 + i % 64] : 0;
-  }
-  if (tid < QPW) sdepth[tid] = (u0 + tid) < a.N ? a.depth[u0 + tid] : 0;
   float bm[BATCH], bl[BATCH], bo[BATCH][DPL];
-  auto load_batch = [&](int g0) {
+  auto load_batch = [&](int g0, int lim_g) {
 #pragma unroll
     for (int t = 0; t < BATCH; ++t) {
       bm[t] = -CH_INF;
       bl[t] = 0.f;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) bo[t][e] = 0.f;
-      if (active && g0 + t < a.G) {  // slots past this step's groups are read but never folded
+      if (g0 + t < lim_g) {
         const int64_t slot = (((int64_t)b * a.H + h) * a.G + g0 + t) * a.N + u;
         bm[t] = a.part_ml[slot * 2];
         bl[t] = a.part_ml[slot * 2 + 1];
@@ -306,46 +293,40 @@ __global__ __launch_bounds__(64 * QPW) void tree_attn_tail(const TreeAttnArgs a)
       }
     }
   };
-  load_batch(0);
+  // slots past this step's groups are read but never folded
+  load_batch(0, a.G);
+
+  // 2. the window rows
+  const int Pu = n + dep;
+  const int p = Pu - WIN + 1 + kw;
+  const int jn = __shfl(pth, min(max(p - n, 0), 63));
+  int e = p < n ? p - (n - WIN) : WIN + jn;  // row-table entry of window key kw
+  if (p < 0) e = WIN + u;                    // u's own slot
+  const long long olo = __shfl(r_lo, e & 63);
+  const long long ohi = __shfl(r_hi, e & (TREE_ATTN_TAIL_ROWS - 64 - 1));
   const int64_t hoff = (int64_t)h * a.ps * HD;
-  for (int rr = tid; rr < ROWS; rr += NT) rowbase[rr] = a.rowtab[(int64_t)b * ROWS + rr] + hoff;
-  const int cmin = n / CHUNK;
-  const int lo = (cmin >= 1 ? cmin - 1 : 0) * CHUNK;  // first staged committed position
-  const int nc = n - lo;                               // committed rows staged (<= 127)
-  const int nrows = nc + a.N;
-  __syncthreads();
-  // 2. V rows -> LDS (float); scores by MFMA -> LDS
+  const int64_t roff = (e < 64 ? olo : ohi) + hoff;
   const T* kpool = (const T*)a.kpool;
   const T* vpool = (const T*)a.vpool;
-  // every load of this phase is issued before any is used: K fragments of
-  // the wave's row tiles (wave w takes tiles w and w + QPW), then V rows
-  constexpr int RT_PER_WAVE = (ROWS / 16 + QPW - 1) / QPW;
-  int4 kf[RT_PER_WAVE][HD / KB];
+  int4 kv[NQ];
 #pragma unroll
-  for (int j = 0; j < RT_PER_WAVE; ++j) {
-    const int rr = 16 * (wave + QPW * j) + c16;  // MFMA B column: staged row
-    const T* kr = kpool + rowbase[rr < nrows ? rr : 0] + g * VEC;
+  for (int i = 0; i < NQ; ++i) kv[i] = ld16(kpool + roff + sub * DPK + i * VEC);
+  T vv[WIN][DPL];
 #pragma unroll
-    for (int ks = 0; ks < HD / KB; ++ks) kf[j][ks] = ld16(kr + ks * KB);
+  for (int k = 0; k < WIN; ++k) {
+    const int64_t ro = __builtin_amdgcn_readlane((int)(roff & 0xffffffff), k * LPK) |
+                       ((int64_t)__builtin_amdgcn_readlane((int)(roff >> 32), k * LPK) << 32);
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) vv[k][d] = vpool[ro + DPL * lane + d];
   }
-  constexpr int UNR = (ROWS * PARTS + NT - 1) / NT;
-  int4 vbuf[UNR];
-#pragma unroll
-  for (int t = 0; t < UNR; ++t) {  // unpredicated: slots past the staged rows re-read row 0
-    const int idx = tid + NT * t;
-    const int rr = idx < nrows * PARTS ? idx / PARTS : 0;
-    vbuf[t] = ld16(vpool + rowbase[rr] + (idx % PARTS) * VEC);
-  }
-  // while those loads are in flight: fold the shared-pass partials of this
-  // wave's query in group order
-  const int Pu = n + sdepth[wave];
-  const int cu = Pu / CHUNK;
+  // while they are in flight: fold the group partials in group order
+  const int lim = Pu - WIN;
+  const int ngrp = lim >= 0 ? (lim / CHUNK) / GROUP + 1 : 0;
   float m = -CH_INF, l = 0.f, o[DPL];
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) o[e] = 0.f;
-  const int lim = cu - 2;
-  const int ngrp = (active && lim >= 0) ? lim / GROUP + 1 : 0;
-  auto fold_batch = [&](int g0) {
+  for (int d = 0; d < DPL; ++d) o[d] = 0.f;
+  for (int g0 = 0; g0 < ngrp; g0 += BATCH) {
+    if (g0 > 0) load_batch(g0, ngrp);
 #pragma unroll
     for (int t = 0; t < BATCH; ++t) {
       if (g0 + t >= ngrp || bm[t] == -CH_INF) continue;
@@ -353,115 +334,47 @@ __global__ __launch_bounds__(64 * QPW) void tree_attn_tail(const TreeAttnArgs a)
       const float a1 = exp_diff(m, mn), a2 = expf(bm[t] - mn);
       l = l * a1 + bl[t] * a2;
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + bo[t][e] * a2;
+      for (int d = 0; d < DPL; ++d) o[d] = o[d] * a1 + bo[t][d] * a2;
       m = mn;
     }
-  };
-  // the first batch was loaded before the K/V requests: straight-line code
-  // here lets its wait leave those in flight
-  fold_batch(0);
-  for (int g0 = BATCH; g0 < ngrp; g0 += BATCH) {
-    load_batch(g0);
-    fold_batch(g0);
   }
-#pragma unroll
-  for (int j = 0; j < RT_PER_WAVE; ++j) {
-    const int rt = wave + QPW * j;
-    if (16 * rt >= nrows) break;  // wave-uniform
-    const int rr = 16 * rt + c16;
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < HD / KB; ++ks) acc = mfma_kb<T>(qf[ks], kf[j][ks], acc);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qi = 4 * g + r;  // output row = query
-      if (qi < QPW && rr < nrows) Sl[qi * ROWS + rr] = acc[r];
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < UNR; ++t) {
-    const int idx = tid + NT * t;
-    if (idx < nrows * PARTS) {
-      const T* ve = reinterpret_cast<const T*>(&vbuf[t]);
-      float* dst = &Vl[(idx / PARTS) * HD + (idx % PARTS) * VEC];
-#pragma unroll
-      for (int e = 0; e < VEC; e += 4)
-        *reinterpret_cast<float4*>(dst + e) =
-            float4{ET<T>::to_f(ve[e]), ET<T>::to_f(ve[e + 1]), ET<T>::to_f(ve[e + 2]), ET<T>::to_f(ve[e + 3])};
-    }
-  }
-  __syncthreads();
-  if (!active) return;
 
-  // 3. per query: the last two chunks, keys in logical-position order
-  const float* srow = Sl + wave * ROWS;
-  // the last two chunks, keys in logical-position order
-  for (int c = (cu >= 1 ? cu - 1 : 0); c <= cu; ++c) {
-    const int p = c * CHUNK + lane;
-    const bool valid = p <= Pu;
-    int row = 0;
-    float s = -CH_INF;
-    if (valid) {
-      row = p < n ? p - lo : nc + (int)spath[wave][p - n];
-      s = srow[row] * a.scale;
-    }
-    // lane 0 holds the chunk's first key, always one of the query's keys
-    const int row0 = __builtin_amdgcn_readlane(row, 0);
-    if (!valid) row = row0;
-    const float mc = wave_max(s);
-    const float mn = fmaxf(m, mc);
-    const float alpha = exp_diff(m, mn);
-    const float pe = valid ? expf(s - mn) : 0.f;
-    l = l * alpha + wave_sum(pe);
+  // 3. the window: each score is a fixed-order dot product over the four
+  // lanes of its key
+  float acc = 0.f;
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) o[e] = o[e] * alpha;
-    // keys in order, 16 per round: the 16 V rows are read before any is used.
-    // Keys past the query's last one in a round have pe = 0 and the staged
-    // row of the chunk's first key, so they add exact zeros.
-    const int cnt = __builtin_amdgcn_readfirstlane(min(CHUNK, Pu - c * CHUNK + 1));
-    for (int i0 = 0; i0 < cnt; i0 += PV_BATCH) {
-      float pis[PV_BATCH];
-      float vv[PV_BATCH][DPL];
+  for (int i = 0; i < NQ; ++i) {
+    const T* qe = reinterpret_cast<const T*>(&qv[i]);
+    const T* ke = reinterpret_cast<const T*>(&kv[i]);
 #pragma unroll
-      for (int j = 0; j < PV_BATCH; ++j) {
-        pis[j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pe), i0 + j));
-        const int ri = __builtin_amdgcn_readlane(row, i0 + j);
-        const float* vr = &Vl[ri * HD + DPL * lane];
+    for (int j = 0; j < VEC; ++j) acc = fmaf(ET<T>::to_f(qe[j]), ET<T>::to_f(ke[j]), acc);
+  }
+  static_assert(LPK == 4, "four lanes per window key");
+  acc = acc + dpp_mov<DPP_XOR1>(acc);
+  acc = acc + dpp_mov<DPP_XOR2>(acc);
+  const bool valid = p >= 0;
+  const float s = valid ? acc * a.scale : -CH_INF;
+  const float mc = wave_max(s);
+  const float mn = fmaxf(m, mc);
+  const float alpha = exp_diff(m, mn);
+  const float pe = valid ? expf(s - mn) : 0.f;
+  l = l * alpha + wave_sum(sub == 0 ? pe : 0.f);
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) vv[j][e] = vr[e];
-      }
+  for (int d = 0; d < DPL; ++d) o[d] = o[d] * alpha;
 #pragma unroll
-      for (int j = 0; j < PV_BATCH; ++j)
+  for (int k = 0; k < WIN; ++k) {
+    const float pk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pe), k * LPK));
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) o[e] = fmaf(pis[j], vv[j][e], o[e]);
-    }
-    m = mn;
+    for (int d = 0; d < DPL; ++d) o[d] = fmaf(pk, ET<T>::to_f(vv[k][d]), o[d]);
   }
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) store_tiled<T>((T*)a.out, a.o_mtiles, b * a.N + u, h * HD + DPL * lane + e, o[e] / l);
-}
-
-template <typename T, int HD, int QPW>
-void tail_go(const TreeAttnArgs& a, hipStream_t st) {
-  const size_t smem = (size_t)(TAIL_ROWS + MAX_NODES) * (HD + QPW) * sizeof(float);
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)tree_attn_tail<T, HD, QPW>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)smem);
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((tree_attn_tail<T, HD, QPW>), dim3((a.N + QPW - 1) / QPW, a.H, a.B), dim3(64 * QPW), smem, st,
-                     a);
+  for (int d = 0; d < DPL; ++d) store_tiled<T>((T*)a.out, a.o_mtiles, b * a.N + u, h * HD + DPL * lane + d, o[d] / l);
 }
 
 template <typename T, int HD>
 void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((tree_attn_shared<T, HD>), dim3(a.G, a.H, a.B), dim3(256), 0, st, a);
-  const int64_t wgs8 = (int64_t)((a.N + TAIL_QPW - 1) / TAIL_QPW) * a.H * a.B;
-  if (wgs8 > 512)
-    tail_go<T, HD, TAIL_QPW_WIDE>(a, st);
-  else
-    tail_go<T, HD, TAIL_QPW>(a, st);
+  hipLaunchKernelGGL((tree_attn_tail<T, HD>), dim3((a.H + 3) / 4, a.N, a.B), dim3(256), 0, st, a);
 }
 
 // ---------------------------------------------------------------------------
