@@ -201,16 +201,21 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
         const int4 hfrag = *reinterpret_cast<const int4*>(ph);
         const int4 mfrag = *reinterpret_cast<const int4*>(pm);
         const int4 lfrag = *reinterpret_cast<const int4*>(pl);
+        int4 vf[HD / 16];
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) {
           const T* vr = &Vt[(16 * db + c16) * VP];
           const int2 lo = *reinterpret_cast<const int2*>(vr + 32 * kp + 4 * g);
           const int2 hi = *reinterpret_cast<const int2*>(vr + 32 * kp + 16 + 4 * g);
-          const int4 vf = int4{lo.x, lo.y, hi.x, hi.y};
-          o[db] = mfma_kb<T>(vf, hfrag, o[db]);
-          o[db] = mfma_kb<T>(vf, mfrag, o[db]);
-          o[db] = mfma_kb<T>(vf, lfrag, o[db]);
+          vf[db] = int4{lo.x, lo.y, hi.x, hi.y};
         }
+        // term-major: consecutive MFMAs update different accumulators
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db) o[db] = mfma_kb<T>(vf[db], hfrag, o[db]);
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db) o[db] = mfma_kb<T>(vf[db], mfrag, o[db]);
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db) o[db] = mfma_kb<T>(vf[db], lfrag, o[db]);
       }
     } else {
 #pragma unroll
