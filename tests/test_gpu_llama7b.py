@@ -3,7 +3,8 @@ V 32000, bf16, 4 draft heads, 64-node tree) in the launch configuration the
 benchmark times.
 
 * Sampled outputs the oracle can compute: teacher-forced steps after a
-  130-token prompt (two shared attention chunks plus the tail), checked
+  130-token prompt (the shared MFMA attention pass over two chunks, a
+  partly masked one, and the 16-position window), checked
   node by node against a float64 oracle holding every 7B weight.
 * Properties that hold at any size, on the benchmark workload itself
   (512-token prompt, forced acceptance p = 0.7), on the 4096-token paged

@@ -557,8 +557,8 @@ def test_small_bf16_branch_drafting_batch_forced(small):
 
 # ---------------------------------------------------------------------------
 # A wide batch: 9 ragged sequences x 32 nodes at 16 heads.  The verify GEMMs
-# take 128-row tiles (the last one partly filled) and the attention tail pass
-# its 16-query workgroups; each sequence is checked against the oracle.
+# take 128-row tiles (the last one partly filled); each sequence is checked
+# against the oracle.
 # ---------------------------------------------------------------------------
 WIDE_CFG = synth.small_config(n_layers=1, d_model=2048, n_heads=16, head_dim=128, d_ffn=1024, vocab=2048,
                               n_draft_heads=4)
