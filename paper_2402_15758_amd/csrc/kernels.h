@@ -56,7 +56,9 @@ struct GemmShape {
   int splits = 1;           // split of the reduction across workgroups
 };
 
-// Splits chosen from (N, K) only, never from M.
+// Splits chosen from (N, K) only, never from M; at most GEMM_MAX_SPLITS (the
+// consumers of split-K partials load them all at once).
+constexpr int GEMM_MAX_SPLITS = 8;
 int gemm_pick_splits(int n_cols, int K, int dtype);
 // ev_start / ev_stop (optional): recorded by the dispatch of the GEMM's
 // first and last kernel (hipExtLaunchKernel), i.e. the kernel execution span.

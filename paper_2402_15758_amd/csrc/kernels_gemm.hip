@@ -471,11 +471,23 @@ __global__ void gemm_finish_kernel(const GemmShape sh, const GemmEpi e, int kind
   const int c16 = (int)(tid & 15);
   const int blk = sh.nb_off + (int)((tid >> 4) % nbc);
   const int row = (int)((tid >> 4) / nbc);
-  float v = 0.f, vp = 0.f;
-  for (int s = 0; s < sh.splits; ++s) {
-    const float* p = part + ((int64_t)s * sh.M + row) * sh.N + 16 * blk;
-    v = (s == 0) ? p[c16] : v + p[c16];
-    vp = (s == 0) ? p[c16 ^ 8] : vp + p[c16 ^ 8];
+  // every slice is requested before the first is added
+  float pv[GEMM_MAX_SPLITS], pp[GEMM_MAX_SPLITS];
+#pragma unroll
+  for (int s = 0; s < GEMM_MAX_SPLITS; ++s) {
+    if (s < sh.splits) {
+      const float* p = part + ((int64_t)s * sh.M + row) * sh.N + 16 * blk;
+      pv[s] = p[c16];
+      pp[s] = p[c16 ^ 8];
+    }
+  }
+  float v = pv[0], vp = pp[0];
+#pragma unroll
+  for (int s = 1; s < GEMM_MAX_SPLITS; ++s) {
+    if (s < sh.splits) {
+      v = v + pv[s];
+      vp = vp + pp[s];
+    }
   }
   epi_elem<T>(e, kind, sh.N, sh.M, 0, row, blk, c16, v, vp);
 }
@@ -583,7 +595,7 @@ int gemm_pick_splits(int n_cols, int K, int dtype) {
   if (n_cols >= SPLIT_MIN_COLS_NO) return 1;
   const int groups = n_cols / 64;
   int s = 1;
-  while (groups * s < SPLIT_TARGET_WGS && s < 8 && kblocks % (2 * s) == 0 && kblocks / (2 * s) >= 16) s *= 2;
+  while (groups * s < SPLIT_TARGET_WGS && s < GEMM_MAX_SPLITS && kblocks % (2 * s) == 0 && kblocks / (2 * s) >= 16) s *= 2;
   return s;
 }
 

@@ -64,8 +64,15 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(float* __restrict__ x, co
   __shared__ float sh[16];
   const int r = blockIdx.x;
   const bool use_alt = alt != nullptr && r >= alt_begin && r < alt_end;
-  float4 v[NV];
+  float4 v[NV], gm[NV];
   float ss = 0.f;
+  // every load is issued before any is used: the gains, the row, and all of
+  // its split-K partials (then summed in slice order)
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = 4 * (threadIdx.x + 1024 * j);
+    gm[j] = i < d ? *reinterpret_cast<const float4*>(gamma + i) : float4{0.f, 0.f, 0.f, 0.f};
+  }
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int i = 4 * (threadIdx.x + 1024 * j);
@@ -75,14 +82,20 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(float* __restrict__ x, co
         val = ld4f<T>(alt + (int64_t)(r - alt_begin) * d + i);
       } else {
         val = *reinterpret_cast<const float4*>(x + (int64_t)r * d + i);
+        float4 pq[GEMM_MAX_SPLITS];
+#pragma unroll
+        for (int q = 0; q < GEMM_MAX_SPLITS; ++q)
+          if (q < n_parts) pq[q] = *reinterpret_cast<const float4*>(parts + ((int64_t)q * M + r) * d + i);
         if (n_parts > 0) {
-          float4 f = *reinterpret_cast<const float4*>(parts + (int64_t)r * d + i);
-          for (int q = 1; q < n_parts; ++q) {
-            const float4 g = *reinterpret_cast<const float4*>(parts + ((int64_t)q * M + r) * d + i);
-            f.x = f.x + g.x;
-            f.y = f.y + g.y;
-            f.z = f.z + g.z;
-            f.w = f.w + g.w;
+          float4 f = pq[0];
+#pragma unroll
+          for (int q = 1; q < GEMM_MAX_SPLITS; ++q) {
+            if (q < n_parts) {
+              f.x = f.x + pq[q].x;
+              f.y = f.y + pq[q].y;
+              f.z = f.z + pq[q].z;
+              f.w = f.w + pq[q].w;
+            }
           }
           val.x = val.x + f.x;
           val.y = val.y + f.y;
@@ -104,12 +117,11 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(float* __restrict__ x, co
   for (int j = 0; j < NV; ++j) {
     const int i = 4 * (threadIdx.x + 1024 * j);
     if (i < d) {
-      const float4 gm = *reinterpret_cast<const float4*>(gamma + i);
       float4 o;
-      o.x = (v[j].x * rinv) * gm.x;
-      o.y = (v[j].y * rinv) * gm.y;
-      o.z = (v[j].z * rinv) * gm.z;
-      o.w = (v[j].w * rinv) * gm.w;
+      o.x = (v[j].x * rinv) * gm[j].x;
+      o.y = (v[j].y * rinv) * gm[j].y;
+      o.z = (v[j].z * rinv) * gm[j].z;
+      o.w = (v[j].w * rinv) * gm[j].w;
       // 4 consecutive columns stay inside one lane's fragment chunk
       st4f<T>(out + tiled_index<T>(o_mtiles, r, i), o);
       if (out_rm != nullptr) st4f<T>(out_rm + (int64_t)r * d + i, o);
@@ -627,8 +639,14 @@ __global__ __launch_bounds__(256) void draft_finish_kernel(StepState s, DraftLev
   const T* hl = (const T*)s.h_last + (int64_t)b * d;
   for (int i = blockIdx.y * 256 + threadIdx.x; i < d; i += gridDim.y * 256) {
     copy_tiled<T>(zin, z_mtiles, r, i, hl[i]);
-    float f = parts[(int64_t)r * d + i];
-    for (int q = 1; q < n_parts; ++q) f = f + parts[((int64_t)q * M + r) * d + i];
+    float pq[GEMM_MAX_SPLITS];  // every slice requested before the first is added
+#pragma unroll
+    for (int q = 0; q < GEMM_MAX_SPLITS; ++q)
+      if (q < n_parts) pq[q] = parts[((int64_t)q * M + r) * d + i];
+    float f = pq[0];
+#pragma unroll
+    for (int q = 1; q < GEMM_MAX_SPLITS; ++q)
+      if (q < n_parts) f = f + pq[q];
     store_tiled<T>(zin, z_mtiles, r, d + i, x[(int64_t)r * d + i] + f);
   }
 }
