@@ -182,3 +182,34 @@ def test_invalid_calls_change_nothing(tiny):
             assert np.array_equal(_bits(u), _bits(v)), (step, key)
     a.close()
     b.close()
+
+
+# Prompt lengths around the attention decomposition's boundaries: the shared
+# MFMA pass takes positions up to P - 16 in 64-position chunks (groups of
+# two), the window the last 16.  Prefill runs chains of up to 64 positions,
+# whose deep nodes read chain positions >= n through the shared pass.
+BOUNDARY_LENS = [12, 13, 16, 17, 47, 48, 62, 63, 64, 65, 77, 78, 79, 80, 81, 125, 126, 127, 128, 129, 143, 144]
+
+
+def test_attention_boundaries(tiny):
+    """For each prompt length: the cache after prefill equals a fresh causal
+    pass (every layer, so layer 1 checks layer 0's attention over the
+    prompt), and three speculative steps match the oracle node by node."""
+    w, orc = tiny
+    log(f"edges: attention boundaries, prompts {BOUNDARY_LENS}")
+    for n0 in BOUNDARY_LENS:
+        prompt = synth.make_prompt(n0, CFG.vocab, 700 + n0)
+        sess = make_session(CFG, w, synth.TREE_T8, max_len=192)
+        first = sess.prefill([prompt])
+        dec = oracle.Decoder(orc, synth.TREE_T8)
+        assert int(first[0]) == dec.prefill(list(prompt)), n0
+        _, _, kv = orc.causal_forward(list(prompt))
+        for layer in range(CFG.n_layers):
+            k, v = sess.kv_read(layer, 0, 0, n0)
+            np.testing.assert_allclose(k, kv[layer][0], rtol=1e-4, atol=1e-5, err_msg=f"K n0={n0} layer {layer}")
+            np.testing.assert_allclose(v, kv[layer][1], rtol=1e-4, atol=1e-5, err_msg=f"V n0={n0} layer {layer}")
+        ties = TieLog()
+        for _ in range(3):
+            check_step(gpu_step(sess), 0, dec, tau(CFG), ties)
+        assert ties.argmax_ties == 0 and ties.list_ties == 0, n0
+        sess.close()
