@@ -188,7 +188,8 @@ def test_invalid_calls_change_nothing(tiny):
 # MFMA pass takes positions up to P - 16 in 64-position chunks (groups of
 # two), the window the last 16.  Prefill runs chains of up to 64 positions,
 # whose deep nodes read chain positions >= n through the shared pass.
-BOUNDARY_LENS = [12, 13, 16, 17, 47, 48, 62, 63, 64, 65, 77, 78, 79, 80, 81, 125, 126, 127, 128, 129, 143, 144]
+BOUNDARY_LENS = [12, 13, 16, 17, 47, 48, 62, 63, 64, 65, 77, 78, 79, 80, 81, 125, 126, 127, 128, 129, 143, 144,
+                 1023, 1024, 1025, 1039, 1040, 1041, 1535, 1536, 1551, 1552]
 
 
 def test_attention_boundaries(tiny):
@@ -199,7 +200,7 @@ def test_attention_boundaries(tiny):
     log(f"edges: attention boundaries, prompts {BOUNDARY_LENS}")
     for n0 in BOUNDARY_LENS:
         prompt = synth.make_prompt(n0, CFG.vocab, 700 + n0)
-        sess = make_session(CFG, w, synth.TREE_T8, max_len=192)
+        sess = make_session(CFG, w, synth.TREE_T8, max_len=max(192, n0 + 64))
         first = sess.prefill([prompt])
         dec = oracle.Decoder(orc, synth.TREE_T8)
         assert int(first[0]) == dec.prefill(list(prompt)), n0
