@@ -319,8 +319,9 @@ __global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
   T vv[WIN][DPL];
 #pragma unroll
   for (int k = 0; k < WIN; ++k) {
-    const int64_t ro = __builtin_amdgcn_readlane((int)(roff & 0xffffffff), k * LPK) |
-                       ((int64_t)__builtin_amdgcn_readlane((int)(roff >> 32), k * LPK) << 32);
+    const uint32_t ro_lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)roff, k * LPK);
+    const int64_t ro = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(roff >> 32), k * LPK) << 32) |
+                                 (uint64_t)ro_lo);
 #pragma unroll
     for (int d = 0; d < DPL; ++d) vv[k][d] = vpool[ro + DPL * lane + d];
   }
