@@ -158,6 +158,19 @@ __device__ __forceinline__ void block_best(float& v, int& i, float* shv, int* sh
     }
 }
 
+// Best (value, id) over the 64 lanes of a wave, on every lane.
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(v, m);
+    const int oi = __shfl_xor(i, m);
+    if (better(ov, oi, v, i)) {
+      v = ov;
+      i = oi;
+    }
+  }
+}
+
 __global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ logits, int V, int* __restrict__ amax) {
   __shared__ float shv[16];
   __shared__ int shi[16];
@@ -201,8 +214,8 @@ __device__ __forceinline__ int forced_ref(const StepState& s, int b, int level, 
 __global__ __launch_bounds__(256) void topk_partial_kernel(const float* __restrict__ logits, int64_t ld, StepState s,
                                                            DraftLevel dl, float* __restrict__ pv,
                                                            int* __restrict__ pi) {
-  __shared__ float shv[4];
-  __shared__ int shi[4];
+  __shared__ float shv[4 * SMAX];
+  __shared__ int shi[4 * SMAX];
   const int split = blockIdx.x, r = blockIdx.y, b = r / dl.R;
   const int V = s.V, level = dl.level;
   const int S = s.s_k[level];
@@ -217,26 +230,38 @@ __global__ __launch_bounds__(256) void topk_partial_kernel(const float* __restri
     lv[q] = -CH_INF;
     li[q] = 0x7fffffff;
   }
-  for (int i = lo + threadIdx.x; i < hi; i += 256) {
-    if (i == excl) continue;
-    float v = z[i];
-    v = (v != v) ? -CH_INF : v;
-    if (!better(v, i, lv[SMAX - 1], li[SMAX - 1])) continue;
-    // insert into the sorted local list
-    float cv = v;
-    int ci = i;
+  // PT values per thread are requested before any is compared
+  constexpr int PT = 4;
+  for (int base = lo + threadIdx.x; base < hi; base += 256 * PT) {
+    float zv[PT];
 #pragma unroll
-    for (int q = 0; q < SMAX; ++q) {
-      if (better(cv, ci, lv[q], li[q])) {
-        const float tv = lv[q];
-        const int ti = li[q];
-        lv[q] = cv;
-        li[q] = ci;
-        cv = tv;
-        ci = ti;
+    for (int t = 0; t < PT; ++t) zv[t] = base + 256 * t < hi ? z[base + 256 * t] : -CH_INF;
+#pragma unroll
+    for (int t = 0; t < PT; ++t) {
+      const int i = base + 256 * t;
+      if (i >= hi || i == excl) continue;
+      float v = zv[t];
+      v = (v != v) ? -CH_INF : v;
+      if (!better(v, i, lv[SMAX - 1], li[SMAX - 1])) continue;
+      // insert into the sorted local list
+      float cv = v;
+      int ci = i;
+#pragma unroll
+      for (int q = 0; q < SMAX; ++q) {
+        if (better(cv, ci, lv[q], li[q])) {
+          const float tv = lv[q];
+          const int ti = li[q];
+          lv[q] = cv;
+          li[q] = ci;
+          cv = tv;
+          ci = ti;
+        }
       }
     }
   }
+  // each wave's best S from its lanes' sorted lists, then the workgroup's
+  // best S from the waves' 4 S candidates (one barrier)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int head = 0;
   for (int q = 0; q < S; ++q) {
     float hv = -CH_INF;
@@ -249,9 +274,30 @@ __global__ __launch_bounds__(256) void topk_partial_kernel(const float* __restri
       }
     float bv = hv;
     int bi = hi_;
-    block_best(bv, bi, shv, shi);
+    wave_best(bv, bi);
     if (bi == hi_ && hi_ != 0x7fffffff) ++head;
-    if (threadIdx.x == 0) {
+    if (lane == 0) {
+      shv[wave * SMAX + q] = bv;
+      shi[wave * SMAX + q] = bi;
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  float cv = -CH_INF;
+  int ci = 0x7fffffff;
+  if (lane < 4 * S) {
+    cv = shv[(lane / S) * SMAX + lane % S];
+    ci = shi[(lane / S) * SMAX + lane % S];
+  }
+  for (int q = 0; q < S; ++q) {
+    float bv = cv;
+    int bi = ci;
+    wave_best(bv, bi);
+    if (bi == ci && ci != 0x7fffffff) {
+      cv = -CH_INF;
+      ci = 0x7fffffff;
+    }
+    if (lane == 0) {
       pv[((int64_t)r * TOPK_SPLIT + split) * SMAX + q] = bv;
       pi[((int64_t)r * TOPK_SPLIT + split) * SMAX + q] = bi;
     }
