@@ -33,6 +33,7 @@ constexpr int NB = 4;        // 16-column blocks per weight-layout group
 constexpr int CB_MAX = 8;    // column blocks per workgroup, upper bound
 constexpr int RED_TILES = 32;  // 16x16 output tiles per wave in one LDS reduction round (4 x 32 KiB)
 constexpr int GEMM_WGS = 256;  // one workgroup per CU per reduction slice
+constexpr int GEMM_XCDS = 8;   // accelerator dies; workgroups are dealt to them round-robin
 // Matrices at least this wide run unsplit (their epilogue needs whole sums and
 // they fill the GPU on their own); narrower ones split the reduction until a
 // launch has at least SPLIT_TARGET_WGS 64-column groups' worth of work.
@@ -202,7 +203,7 @@ __device__ __forceinline__ int4 ldw(const T* p) {
 template <typename T, int MB, int CB, int J0, int JN>
 __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0,
                                               const f32x4 (&acc)[MB][CB], f32x4* red, const RowMeta* rm,
-                                              float* stage, int wave, int lane) {
+                                              float* stage, int wave, int lane, int split) {
   const int g = lane >> 4, c16 = lane & 15;
 #pragma unroll
   for (int i = 0; i < MB; ++i)
@@ -292,7 +293,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
       base = e.out_f;
       ld = e.ldo;
     } else {
-      base = e.part + (int64_t)blockIdx.z * sh.M * sh.N;
+      base = e.part + (int64_t)split * sh.M * sh.N;
       ld = sh.N;
     }
 #pragma unroll
@@ -344,14 +345,14 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
     for (int r = 0; r < 4; ++r) {
       const int row = 16 * (mb0 + i) + 4 * g + r;
       if (it < MB * JN && row < sh.M)
-        epi_elem<T>(e, kind, sh.N, sh.M, blockIdx.z, row, cb0 + j, c16, vv[k][r], vpp[k][r]);
+        epi_elem<T>(e, kind, sh.N, sh.M, split, row, cb0 + j, c16, vv[k][r], vpp[k][r]);
     }
   }
 }
 
 template <typename T, int MB, int CB, int PF>
 __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, int kind, int cb0, int mb0, int kbeg,
-                                         int kend, f32x4* red, const RowMeta* rm, float* stage) {
+                                         int kend, f32x4* red, const RowMeta* rm, float* stage, int split) {
   constexpr int VEC = ET<T>::VEC;
   // The wave index is made provably wave-uniform so that every branch of the
   // k-loop below is a scalar branch: an MFMA ignores EXEC, so it must never
@@ -419,27 +420,46 @@ __device__ __forceinline__ void gemm_run(const GemmShape& sh, const GemmEpi& e, 
 
   // the four waves' partial sums meet in LDS, JR column blocks at a time
   constexpr int JR = CB < RED_TILES / MB ? CB : RED_TILES / MB;
-  gemm_epilogue<T, MB, CB, 0, JR>(sh, e, kind, cb0, mb0, acc, red, rm, stage, wave, lane);
+  gemm_epilogue<T, MB, CB, 0, JR>(sh, e, kind, cb0, mb0, acc, red, rm, stage, wave, lane, split);
   if constexpr (CB > JR) {
     __syncthreads();  // the first round's reads of red are done
-    gemm_epilogue<T, MB, CB, JR, CB - JR>(sh, e, kind, cb0, mb0, acc, red, rm, stage, wave, lane);
+    gemm_epilogue<T, MB, CB, JR, CB - JR>(sh, e, kind, cb0, mb0, acc, red, rm, stage, wave, lane, split);
   }
+}
+
+// Workgroup -> (row block, column run, split).  Workgroups are dealt to the
+// 8 XCDs round-robin by linear id.  When a launch has several row blocks and
+// its (run, split) count is a multiple of 8, consecutive workgroups of one
+// XCD take the row blocks of one weight run, so every run's weight tiles are
+// fetched from HBM once into that XCD's L2 and re-read from there; otherwise
+// the linear order is used.  The mapping moves no arithmetic.
+struct GemmTile {
+  int rb, run, split;
+};
+// X, Y: grid.x and grid.y (X > 1 and grid.y * grid.z a multiple of 8).
+__device__ __forceinline__ GemmTile gemm_tile_xcd(int X, int Y) {
+  const int L = blockIdx.x + X * (blockIdx.y + Y * blockIdx.z);  // linear dispatch id
+  const int xcd = L % GEMM_XCDS, k = L / GEMM_XCDS;
+  const int r = (k / X) * GEMM_XCDS + xcd;
+  return GemmTile{k % X, r % Y, r / Y};
 }
 
 // grid = (row blocks of 16 MB, workgroups per slice, splits).  Workgroups
 // [0, nbig) own CBA column blocks, the others CBA - 1.
-template <typename T, int MB, int CBA>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const GemmEpi e, int kind, int nbig) {
+template <typename T, int MB, int CBA, bool XCD_MAP>
+__global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const GemmEpi e, int kind, int nbig, int gx,
+                                                   int gy) {
   constexpr int PF = MB == 1 ? 4 : (MB >= 8 ? 2 : 3);
   constexpr int JR = CBA < RED_TILES / MB ? CBA : RED_TILES / MB;
   if (sh.skip && *sh.skip == 0) return;
   __shared__ f32x4 red[4 * MB * JR * 64];
   const int kblocks = sh.K / (4 * ET<T>::VEC);
   const int kps = kblocks / sh.splits;
-  const int kbeg = blockIdx.z * kps;
+  const GemmTile tl = XCD_MAP ? gemm_tile_xcd(gx, gy) : GemmTile{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+  const int kbeg = tl.split * kps;
   const int kend = kbeg + kps;
-  const int b = blockIdx.y;
-  const int mb0 = blockIdx.x * MB;
+  const int b = tl.run;
+  const int mb0 = tl.rb * MB;
   // QKV epilogue targets of this workgroup's rows (visible after the k-loop's
   // barrier)
   __shared__ RowMeta rm[16 * MB];
@@ -451,11 +471,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmShape sh, const Gem
     rm[threadIdx.x] = t;
   }
   if (b < nbig) {
-    gemm_run<T, MB, CBA, PF>(sh, e, kind, sh.nb_off + b * CBA, mb0, kbeg, kend, red, rm, stage);
+    gemm_run<T, MB, CBA, PF>(sh, e, kind, sh.nb_off + b * CBA, mb0, kbeg, kend, red, rm, stage, tl.split);
   } else {
     if constexpr (CBA > 1)
       gemm_run<T, MB, CBA - 1, PF>(sh, e, kind, sh.nb_off + nbig * CBA + (b - nbig) * (CBA - 1), mb0, kbeg, kend,
-                                   red, rm, stage);
+                                   red, rm, stage, tl.split);
   }
 }
 
@@ -496,10 +516,22 @@ template <typename T, int MB, int CBA>
 void gemm_launch(const GemmShape& s, const GemmEpi& e, int kind, int nwg, int nbig, hipStream_t st, hipEvent_t ea,
                  hipEvent_t eb) {
   dim3 grid((s.M + 16 * MB - 1) / (16 * MB), nwg, s.splits);
+  const int gx = (int)grid.x, gy = (int)grid.y;
+  if (gx > 1 && (gy * s.splits) % GEMM_XCDS == 0) {
+    if constexpr (MB > 1) {
+      if (ea || eb)
+        hipExtLaunchKernelGGL((gemm_kernel<T, MB, CBA, true>), grid, dim3(256), 0, st, ea, eb, 0, s, e, kind, nbig, gx,
+                              gy);
+      else
+        hipLaunchKernelGGL((gemm_kernel<T, MB, CBA, true>), grid, dim3(256), 0, st, s, e, kind, nbig, gx, gy);
+      return;
+    }
+  }
   if (ea || eb)
-    hipExtLaunchKernelGGL((gemm_kernel<T, MB, CBA>), grid, dim3(256), 0, st, ea, eb, 0, s, e, kind, nbig);
+    hipExtLaunchKernelGGL((gemm_kernel<T, MB, CBA, false>), grid, dim3(256), 0, st, ea, eb, 0, s, e, kind, nbig, gx,
+                          gy);
   else
-    hipLaunchKernelGGL((gemm_kernel<T, MB, CBA>), grid, dim3(256), 0, st, s, e, kind, nbig);
+    hipLaunchKernelGGL((gemm_kernel<T, MB, CBA, false>), grid, dim3(256), 0, st, s, e, kind, nbig, gx, gy);
 }
 
 template <typename T, int MB>
