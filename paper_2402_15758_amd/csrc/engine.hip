@@ -768,7 +768,7 @@ void ctx_dims(chimera_ctx* c) {
   // drafted nodes (branch-conditioned drafting), fewer than N per sequence
   c->Mq = c->B * std::max(c->N - 1, 1);
   c->Md = mcap(std::max({c->B * (2 * (c->K + 1) + 1), c->Mq, 128}));
-  c->G = (c->kv->max_len + TREE_ATTN_GROUP_POSITIONS - 1) / TREE_ATTN_GROUP_POSITIONS + 1;
+  c->G = tree_attn_groups(c->kv->max_len);
   c->tok_stride = c->kv->max_len + 8;
   c->nblk_enc = (2 * c->kv->cap + cf.n_draft_heads + 1 + 255) / 256;
 }

@@ -81,8 +81,17 @@ void launch_rmsnorm(int dtype, float* x, const float* parts, int n_parts, const 
 
 // ---- attention ---------------------------------------------------------------
 // The shared pass of the tree attention writes one partial per group of
-// this many committed positions (2 chunks of 64).
-constexpr int TREE_ATTN_GROUP_POSITIONS = 128;
+// 64-position chunks.  Groups are fixed by absolute chunk index: chunks
+// 0 .. TREE_ATTN_NEAR_CHUNKS-1 form pairs; later chunks form groups of
+// TREE_ATTN_FAR_GROUP (fewer partials where contexts are long).
+constexpr int TREE_ATTN_NEAR_CHUNKS = 16;
+constexpr int TREE_ATTN_FAR_GROUP = 4;
+// Group slots covering positions 0 .. max_len - 1.
+inline int tree_attn_groups(int max_len) {
+  const int chunks = (max_len + 63) / 64;
+  if (chunks <= TREE_ATTN_NEAR_CHUNKS) return (chunks + 1) / 2;
+  return TREE_ATTN_NEAR_CHUNKS / 2 + (chunks - TREE_ATTN_NEAR_CHUNKS + TREE_ATTN_FAR_GROUP - 1) / TREE_ATTN_FAR_GROUP;
+}
 struct TreeAttnArgs {
   const void* q;            // [B*N][ldq] rotated queries
   int ldq;
@@ -98,7 +107,7 @@ struct TreeAttnArgs {
   float scale;
   float* part_o;            // [B][H][G][N][hd]
   float* part_ml;           // [B][H][G][N][2]
-  int G;                    // group slots (groups of TREE_ATTN_GROUP_POSITIONS positions)
+  int G;                    // group slots (tree_attn_groups)
   void* out;                // tiled [B*N][H*hd] with o_mtiles tiles
   int o_mtiles;
   int B;

@@ -7,9 +7,10 @@
 // keys are reduced with the online softmax in two parts, folded in order:
 //   * positions 0 .. P_u - W (W = TREE_ATTN_WINDOW, deeper than any tree)
 //     are committed keys, shared by every query of the tree: an MFMA pass
-//     over 64-position chunks aligned to position 0, in groups of two
-//     chunks, writes one partial (m, l, O) per group, each query masking
-//     the keys past its own bound;
+//     over 64-position chunks aligned to position 0, in groups fixed by
+//     chunk index (pairs, then groups of four past the first 16 chunks),
+//     writes one partial (m, l, O) per group, each query masking the keys
+//     past its own bound;
 //   * the window P_u - W + 1 .. P_u, which holds every tree position, is
 //     reduced per query (one wave per query and head) after folding the
 //     group partials in group order.
@@ -22,7 +23,14 @@
 namespace {
 
 constexpr int CHUNK = 64;   // positions per chunk
-constexpr int GROUP = TREE_ATTN_GROUP_POSITIONS / CHUNK;  // chunks per shared-pass workgroup
+constexpr int NEAR = TREE_ATTN_NEAR_CHUNKS;
+constexpr int FAR = TREE_ATTN_FAR_GROUP;
+constexpr int GMAX = FAR > 2 ? FAR : 2;  // chunks per group, upper bound
+static_assert(NEAR % 2 == 0, "near chunks form pairs");
+// Group of chunk c, and the first chunk and chunk count of group g.
+__device__ __forceinline__ int group_of_chunk(int c) { return c < NEAR ? c / 2 : NEAR / 2 + (c - NEAR) / FAR; }
+__device__ __forceinline__ int group_first_chunk(int g) { return g < NEAR / 2 ? 2 * g : NEAR + (g - NEAR / 2) * FAR; }
+__device__ __forceinline__ int group_chunks(int g) { return g < NEAR / 2 ? 2 : FAR; }
 constexpr int WIN = TREE_ATTN_WINDOW;  // window positions reduced per query
 constexpr int MAX_NODES = 64;
 static_assert(WIN + MAX_NODES == TREE_ATTN_TAIL_ROWS, "window rows");
@@ -56,7 +64,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   __shared__ __attribute__((aligned(16))) T Ks[CHUNK * KP];
   __shared__ __attribute__((aligned(16))) T Vt[HD * VP];
 
-  __shared__ int64_t pbase[GROUP * CHUNK];  // element offset of each staged key's row
+  __shared__ int64_t pbase[GMAX * CHUNK];  // element offset of each staged key's row
   const int grp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   // wave-uniform wave index: the MFMAs below sit under wave-level branches only
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -75,18 +83,19 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   const int dep_u = a.depth[uu];
   const int n = a.n_b[b];
   // the group's page ids need no n: load them with it
-  const int c_begin = grp * GROUP;
-  constexpr int PB = (GROUP * CHUNK + 255) / 256;
+  const int c_begin = group_first_chunk(grp);
+  const int nch = group_chunks(grp);
+  constexpr int PB = (GMAX * CHUNK + 255) / 256;
   int pg[PB];
 #pragma unroll
   for (int t = 0; t < PB; ++t) {
     const int i = tid + 256 * t;
     const int pi = (c_begin * CHUNK + i) / a.ps;
-    pg[t] = (i < GROUP * CHUNK && pi < a.max_pages) ? a.page_table[(int64_t)b * a.max_pages + pi] : 0;
+    pg[t] = (i < nch * CHUNK && pi < a.max_pages) ? a.page_table[(int64_t)b * a.max_pages + pi] : 0;
   }
   const int maxk = n + a.D - WIN;        // last position any query treats as shared
   if (maxk < 0 || c_begin > maxk / CHUNK) return;
-  const int c_end = min(c_begin + GROUP - 1, maxk / CHUNK);
+  const int c_end = min(c_begin + nch - 1, maxk / CHUNK);
   const int lim_u = n + dep_u - WIN;    // query u's last shared position
   // rows past the ones written so far (positions >= n + N) may hold
   // anything: they are staged as zeros, so masked keys add exact zeros
@@ -95,7 +104,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   for (int t = 0; t < PB; ++t) {
     const int i = tid + 256 * t;
     const int p = c_begin * CHUNK + i;
-    if (i < GROUP * CHUNK) pbase[i] = (int64_t)pg[t] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD;
+    if (i < nch * CHUNK) pbase[i] = (int64_t)pg[t] * a.page_stride + ((int64_t)h * a.ps + p % a.ps) * HD;
   }
   __syncthreads();
   float m = -CH_INF, l = 0.f;
@@ -327,7 +336,7 @@ __global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
   }
   // while they are in flight: fold the group partials in group order
   const int lim = Pu - WIN;
-  const int ngrp = lim >= 0 ? (lim / CHUNK) / GROUP + 1 : 0;
+  const int ngrp = lim >= 0 ? group_of_chunk(lim / CHUNK) + 1 : 0;
   float m = -CH_INF, l = 0.f, o[DPL];
 #pragma unroll
   for (int d = 0; d < DPL; ++d) o[d] = 0.f;

@@ -185,11 +185,11 @@ def test_invalid_calls_change_nothing(tiny):
 
 
 # Prompt lengths around the attention decomposition's boundaries: the shared
-# MFMA pass takes positions up to P - 16 in 64-position chunks (groups of
-# two), the window the last 16.  Prefill runs chains of up to 64 positions,
+# MFMA pass takes positions up to P - 16 in 64-position chunks (pairs below
+# position 1024, groups of four beyond), the window the last 16.  Prefill runs chains of up to 64 positions,
 # whose deep nodes read chain positions >= n through the shared pass.
 BOUNDARY_LENS = [12, 13, 16, 17, 47, 48, 62, 63, 64, 65, 77, 78, 79, 80, 81, 125, 126, 127, 128, 129, 143, 144,
-                 1023, 1024, 1025, 1039, 1040, 1041, 1535, 1536, 1551, 1552]
+                 1023, 1024, 1025, 1039, 1040, 1041, 1295, 1296, 1297, 1535, 1536, 1551, 1552]
 
 
 def test_attention_boundaries(tiny):
