@@ -17,13 +17,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
 
-// float -> bf16, round to nearest, ties to even (NaN -> quiet NaN).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// float -> bf16, round to nearest, ties to even (NaN -> quiet NaN): gfx950's
+// v_cvt_pk_bf16_f32, with denormals preserved (the kernels' float mode).
+__device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 // Storage-type traits.  A "fragment" is the 16 bytes one lane feeds into a
 // 16x16 MFMA k-block: VEC consecutive elements along the reduction axis.
