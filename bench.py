@@ -128,14 +128,19 @@ def cpu_baseline(wl, weights_gpu, prompt, accept_len):
 
 def counter_traffic():
     """HBM bytes per verify-GEMM launch from the committed rocprofv3 counter
-    summary, if the GEMM source still has the hash it was measured with."""
+    summary, if the GEMM's sources (the kernel file and the headers it
+    includes) still have the hash they were measured with."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "verify_gemm_llama7b_p512_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = os.path.join(ROOT, rec["source"])
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+    if "sources" not in rec:
+        return None
+    h = hashlib.sha256()
+    for src in rec["sources"]:
+        h.update(open(os.path.join(ROOT, src), "rb").read())
+    if h.hexdigest() != rec["sources_sha256"]:
         return None
     return rec["traffic_bytes_per_launch"]
 
