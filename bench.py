@@ -128,8 +128,9 @@ def cpu_baseline(wl, weights_gpu, prompt, accept_len):
 
 def counter_traffic():
     """HBM bytes per verify-GEMM launch from the committed rocprofv3 counter
-    summary, if the GEMM's sources (the kernel file and the headers it
-    includes) still have the hash they were measured with."""
+    summary, if the GEMM's sources (the kernel file, the headers it
+    includes and the build script with its compiler flags) still have the
+    hash they were measured with."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "verify_gemm_llama7b_p512_traffic.json")
     if not os.path.exists(path):
