@@ -265,7 +265,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 // read u's own slot and add exact zeros.
 // ---------------------------------------------------------------------------
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
+__global__ __launch_bounds__(256) void tree_attn_window(const TreeAttnArgs a) {
   constexpr int VEC = ET<T>::VEC;
   constexpr int DPL = HD / 64;   // output dims per lane
   constexpr int LPK = 64 / WIN;  // lanes per window key
@@ -389,7 +389,7 @@ __global__ __launch_bounds__(256) void tree_attn_tail(const TreeAttnArgs a) {
 template <typename T, int HD>
 void tree_attn_go(const TreeAttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((tree_attn_shared<T, HD>), dim3(a.G, a.H, a.B), dim3(256), 0, st, a);
-  hipLaunchKernelGGL((tree_attn_tail<T, HD>), dim3((a.H + 3) / 4, a.N, a.B), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((tree_attn_window<T, HD>), dim3((a.H + 3) / 4, a.N, a.B), dim3(256), 0, st, a);
 }
 
 // ---------------------------------------------------------------------------
