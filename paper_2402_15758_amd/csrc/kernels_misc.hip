@@ -13,7 +13,23 @@ __global__ void embed_kernel(const int* __restrict__ tokens, const T* __restrict
   const int r = blockIdx.x;
   const int t = min(max(tokens[r], 0), V - 1);
   const T* e = E + (int64_t)t * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) x[(int64_t)r * d + i] = ET<T>::to_f(e[i]);
+  float* xr = x + (int64_t)r * d;
+  constexpr int VEC = ET<T>::VEC, U = 4;  // 16-byte pieces, U per thread requested at once
+  const int pieces = d / VEC;
+  for (int p0 = threadIdx.x; p0 < pieces; p0 += U * 256) {
+    int4 buf[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (p0 + 256 * u < pieces) buf[u] = ld16(e + (int64_t)(p0 + 256 * u) * VEC);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (p0 + 256 * u >= pieces) break;
+      const T* v = reinterpret_cast<const T*>(&buf[u]);
+#pragma unroll
+      for (int k = 0; k < VEC; ++k) xr[(p0 + 256 * u) * VEC + k] = ET<T>::to_f(v[k]);
+    }
+  }
+  for (int i = pieces * VEC + threadIdx.x; i < d; i += 256) xr[i] = ET<T>::to_f(e[i]);  // d % VEC tail
 }
 
 // Fixed-order block sum: wave butterflies, then the waves in order.
@@ -178,15 +194,24 @@ __global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ 
   const float* z = logits + (int64_t)r * V;
   float bv = -CH_INF;
   int bi = 0x7fffffff;
-  for (int i4 = threadIdx.x; 4 * i4 < V; i4 += 1024) {
-    const float4 q = *reinterpret_cast<const float4*>(z + 4 * i4);
-    const float e[4] = {q.x, q.y, q.z, q.w};
+  constexpr int U = 8;  // float4 pieces per thread requested at once
+  for (int b4 = threadIdx.x; 4 * b4 < V; b4 += U * 1024) {
+    float4 q[U];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float v = (e[k] != e[k]) ? -CH_INF : e[k];
-      if (better(v, 4 * i4 + k, bv, bi)) {
-        bv = v;
-        bi = 4 * i4 + k;
+    for (int u = 0; u < U; ++u)
+      if (4 * (b4 + 1024 * u) < V) q[u] = *reinterpret_cast<const float4*>(z + 4 * (b4 + 1024 * u));
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i4 = b4 + 1024 * u;
+      if (4 * i4 >= V) break;
+      const float e[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float v = (e[k] != e[k]) ? -CH_INF : e[k];
+        if (better(v, 4 * i4 + k, bv, bi)) {
+          bv = v;
+          bi = 4 * i4 + k;
+        }
       }
     }
   }
