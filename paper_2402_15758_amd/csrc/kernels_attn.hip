@@ -32,6 +32,13 @@ __device__ __forceinline__ int group_of_chunk(int c) { return c < NEAR ? c / 2 :
 __device__ __forceinline__ int group_first_chunk(int g) { return g < NEAR / 2 ? 2 * g : NEAR + (g - NEAR / 2) * FAR; }
 __device__ __forceinline__ int group_chunks(int g) { return g < NEAR / 2 ? 2 : FAR; }
 constexpr int WIN = TREE_ATTN_WINDOW;  // window positions reduced per query
+// The tree attention's softmax runs in base 2 on scores pre-scaled by
+// log2(e) (exp(x) = 2^(x log2 e)), with gfx950's v_exp_f32; partials keep
+// their maxima in that scale.
+constexpr float LOG2E = 1.44269504088896340736f;
+__device__ __forceinline__ float exp2_diff(float a, float b) {
+  return a == -CH_INF ? 0.0f : __builtin_amdgcn_exp2f(a - b);
+}
 constexpr int MAX_NODES = 64;
 static_assert(WIN + MAX_NODES == TREE_ATTN_TAIL_ROWS, "window rows");
 static_assert(WIN == 16, "the window pass maps four lanes to each window key");
@@ -108,6 +115,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   }
   __syncthreads();
   float m = -CH_INF, l = 0.f;
+  const float scale2 = a.scale * LOG2E;
   f32x4 o[HD / 16];
 #pragma unroll
   for (int db = 0; db < HD / 16; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -164,7 +172,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const bool act = valid_u && c * CHUNK + 16 * kb + 4 * g + r <= lim_u;  // S^T row = key
-        const float v = act ? s[kb][r] * a.scale : -CH_INF;
+        const float v = act ? s[kb][r] * scale2 : -CH_INF;
         s[kb][r] = v;
         mc = fmaxf(mc, v);
       }
@@ -172,12 +180,12 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
     const float mn = fmaxf(m, mc);
     float alpha = 1.f, ls = 0.f;
     if (mn != -CH_INF) {
-      alpha = exp_diff(m, mn);
+      alpha = exp2_diff(m, mn);
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = exp_diff(s[kb][r], mn);
+          const float p = exp2_diff(s[kb][r], mn);
           s[kb][r] = p;
           ls = ls + p;
         }
@@ -346,7 +354,7 @@ __global__ __launch_bounds__(256) void tree_attn_window(const TreeAttnArgs a) {
     for (int t = 0; t < BATCH; ++t) {
       if (g0 + t >= ngrp || bm[t] == -CH_INF) continue;
       const float mn = fmaxf(m, bm[t]);
-      const float a1 = exp_diff(m, mn), a2 = expf(bm[t] - mn);
+      const float a1 = exp2_diff(m, mn), a2 = __builtin_amdgcn_exp2f(bm[t] - mn);
       l = l * a1 + bl[t] * a2;
 #pragma unroll
       for (int d = 0; d < DPL; ++d) o[d] = o[d] * a1 + bo[t][d] * a2;
@@ -368,11 +376,11 @@ __global__ __launch_bounds__(256) void tree_attn_window(const TreeAttnArgs a) {
   acc = acc + dpp_mov<DPP_XOR1>(acc);
   acc = acc + dpp_mov<DPP_XOR2>(acc);
   const bool valid = p >= 0;
-  const float s = valid ? acc * a.scale : -CH_INF;
+  const float s = valid ? acc * (a.scale * LOG2E) : -CH_INF;
   const float mc = wave_max(s);
   const float mn = fmaxf(m, mc);
-  const float alpha = exp_diff(m, mn);
-  const float pe = valid ? expf(s - mn) : 0.f;
+  const float alpha = exp2_diff(m, mn);
+  const float pe = valid ? __builtin_amdgcn_exp2f(s - mn) : 0.f;
   l = l * alpha + wave_sum(sub == 0 ? pe : 0.f);
 #pragma unroll
   for (int d = 0; d < DPL; ++d) o[d] = o[d] * alpha;
