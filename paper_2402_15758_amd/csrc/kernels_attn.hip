@@ -516,16 +516,34 @@ __global__ void enc_attn_combine(const EncAttnArgs a) {
   float m = -CH_INF, l = 0.f, o[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) o[e] = 0.f;
-  for (int blk = 0; blk < used; ++blk) {
-    const float* src = a.part + (((int64_t)row * a.H + h) * a.nblk + blk) * (HD + 2);
-    const float mg = src[HD], lg = src[HD + 1];
-    if (mg == -CH_INF) continue;
-    const float mn = fmaxf(m, mg);
-    const float a1 = exp_diff(m, mn), a2 = expf(mg - mn);
-    l = l * a1 + lg * a2;
+  // block partials are requested CB at a time, then folded in block order
+  constexpr int CB = 8;
+  for (int b0 = 0; b0 < used; b0 += CB) {
+    float bm[CB], bl[CB], bo[CB][DPL];
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + src[DPL * lane + e] * a2;
-    m = mn;
+    for (int t = 0; t < CB; ++t) {
+      bm[t] = -CH_INF;
+      bl[t] = 0.f;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) bo[t][e] = 0.f;
+      if (b0 + t < used) {
+        const float* src = a.part + (((int64_t)row * a.H + h) * a.nblk + b0 + t) * (HD + 2);
+        bm[t] = src[HD];
+        bl[t] = src[HD + 1];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) bo[t][e] = src[DPL * lane + e];
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < CB; ++t) {
+      if (b0 + t >= used || bm[t] == -CH_INF) continue;
+      const float mn = fmaxf(m, bm[t]);
+      const float a1 = exp_diff(m, mn), a2 = expf(bm[t] - mn);
+      l = l * a1 + bl[t] * a2;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) o[e] = o[e] * a1 + bo[t][e] * a2;
+      m = mn;
+    }
   }
 #pragma unroll
   for (int e = 0; e < DPL; ++e) store_tiled<T>((T*)a.out, a.o_mtiles, row, h * HD + DPL * lane + e, o[e] / l);
