@@ -36,6 +36,13 @@ constexpr int WIN = TREE_ATTN_WINDOW;  // window positions reduced per query
 // log2(e) (exp(x) = 2^(x log2 e)), with gfx950's v_exp_f32; partials keep
 // their maxima in that scale.
 constexpr float LOG2E = 1.44269504088896340736f;
+// Two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32;
+// a in the low half.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, b2));
+}
 __device__ __forceinline__ float exp2_diff(float a, float b) {
   return a == -CH_INF ? 0.0f : __builtin_amdgcn_exp2f(a - b);
 }
@@ -206,18 +213,20 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
       // is as precise as a float dot product
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp) {
-        bf16_t ph[8], pm[8], pl[8];
+        // fragment element e is s[2 kp + e / 4][e % 4]; two elements per
+        // conversion, element 2q in the low half of word q
+        uint32_t ph[4], pm[4], pl[4];
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          const float pv = s[2 * kp + r / 4][r % 4];
-          ph[r] = f2bf(pv);
-          const float r1 = pv - bf2f(ph[r]);
-          pm[r] = f2bf(r1);
-          pl[r] = f2bf(r1 - bf2f(pm[r]));
+        for (int q = 0; q < 4; ++q) {
+          const float a0 = s[2 * kp + q / 2][2 * (q % 2)], a1 = s[2 * kp + q / 2][2 * (q % 2) + 1];
+          ph[q] = cvt_pk_bf16(a0, a1);
+          const float r0 = a0 - __uint_as_float(ph[q] << 16), r1 = a1 - __uint_as_float(ph[q] & 0xffff0000u);
+          pm[q] = cvt_pk_bf16(r0, r1);
+          pl[q] = cvt_pk_bf16(r0 - __uint_as_float(pm[q] << 16), r1 - __uint_as_float(pm[q] & 0xffff0000u));
         }
-        const int4 hfrag = *reinterpret_cast<const int4*>(ph);
-        const int4 mfrag = *reinterpret_cast<const int4*>(pm);
-        const int4 lfrag = *reinterpret_cast<const int4*>(pl);
+        const int4 hfrag = int4{(int)ph[0], (int)ph[1], (int)ph[2], (int)ph[3]};
+        const int4 mfrag = int4{(int)pm[0], (int)pm[1], (int)pm[2], (int)pm[3]};
+        const int4 lfrag = int4{(int)pl[0], (int)pl[1], (int)pl[2], (int)pl[3]};
         int4 vf[HD / 16];
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) {
