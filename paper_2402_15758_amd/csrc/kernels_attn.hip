@@ -75,6 +75,7 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   constexpr int VEC = ET<T>::VEC, KB = 4 * VEC;
   constexpr int KP = HD + VEC;         // K row pitch (elements)
   constexpr int VP = CHUNK + VEC;      // V^T row pitch (elements)
+  static_assert(VP % 2 == 0 && CHUNK % 2 == 0, "V^T rows hold whole 32-bit key pairs");
   __shared__ __attribute__((aligned(16))) T Ks[CHUNK * KP];
   __shared__ __attribute__((aligned(16))) T Vt[HD * VP];
 
@@ -157,9 +158,26 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
       st16(&Ks[(idx / PARTS) * KP + (idx % PARTS) * VEC], c * CHUNK + idx / PARTS < wlim ? kreg[t] : zero);
       const int key = idx % CHUNK, part = idx / CHUNK;
       const int4 vk = c * CHUNK + key < wlim ? vreg[t] : zero;
-      const T* ve = reinterpret_cast<const T*>(&vk);
+      if constexpr (sizeof(T) == 2) {
+        // V^T as 32-bit words holding keys (2j, 2j+1): the two lanes (same
+        // wave) swap half of their 8 dims, then the even lane writes dims
+        // 0-3 and the odd lane dims 4-7
+        const bool odd = key & 1;
+        const uint32_t r0 = __builtin_amdgcn_update_dpp(0, odd ? vk.x : vk.z, DPP_XOR1, 0xF, 0xF, false);
+        const uint32_t r1 = __builtin_amdgcn_update_dpp(0, odd ? vk.y : vk.w, DPP_XOR1, 0xF, 0xF, false);
+        const uint32_t m0 = odd ? vk.z : vk.x, m1 = odd ? vk.w : vk.y;  // own dims, two per word
+        const uint32_t lo0 = odd ? r0 : m0, hi0 = odd ? m0 : r0;        // key 2j, key 2j+1
+        const uint32_t lo1 = odd ? r1 : m1, hi1 = odd ? m1 : r1;
+        uint32_t* vw = reinterpret_cast<uint32_t*>(Vt) + ((part * VEC + (odd ? 4 : 0)) * VP + (key & ~1)) / 2;
+        vw[0] = (lo0 & 0xffffu) | (hi0 << 16);
+        vw[VP / 2] = (lo0 >> 16) | (hi0 & 0xffff0000u);
+        vw[VP] = (lo1 & 0xffffu) | (hi1 << 16);
+        vw[3 * VP / 2] = (lo1 >> 16) | (hi1 & 0xffff0000u);
+      } else {
+        const T* ve = reinterpret_cast<const T*>(&vk);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) Vt[(part * VEC + e) * VP + key] = ve[e];
+        for (int e = 0; e < VEC; ++e) Vt[(part * VEC + e) * VP + key] = ve[e];
+      }
     }
     __syncthreads();
     if (c < c_end) load_chunk(c + 1);
