@@ -149,7 +149,7 @@ def counter_traffic():
 def main():
     a = parse()
     if a.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(the decode step of one sequence batch lives on one MI355X)", file=sys.stderr)
         sys.exit(2)
     import torch
