@@ -121,14 +121,34 @@ def softmax_rows(s: np.ndarray) -> np.ndarray:
     return e / np.sum(e, axis=-1, keepdims=True)
 
 
-def masked_attention(q, k, v, visible):
+def masked_attention(q, k, v, visible, rows_per_block: int = 256):
     """Multi-head scaled dot-product attention.
-    q [M, H, hd]; k, v [P, H, hd]; visible [M, P] bool.  Returns [M, H, hd]."""
-    hd = q.shape[-1]
-    s = np.einsum("mhd,phd->hmp", q, k) / np.sqrt(hd)
-    s = np.where(visible[None, :, :], s, -np.inf)
-    p = softmax_rows(s)
-    return np.einsum("hmp,phd->mhd", p, v)
+    q [M, H, hd]; k, v [P, H, hd]; visible [M, P] bool.  Returns [M, H, hd].
+
+    softmax(q k^T / sqrt(hd)) v per head, over the keys each query may see.
+    Query rows are independent, so they are evaluated in blocks of
+    ``rows_per_block``; a block reads the keys up to the last one any of its
+    rows can see (the keys after it would only add exact zeros)."""
+    M, H, hd = q.shape
+    out = np.zeros((M, H, v.shape[-1]), dtype=np.result_type(q, v))
+    kh = np.ascontiguousarray(np.transpose(k, (1, 2, 0)))  # [H, hd, P]
+    vh = np.ascontiguousarray(np.transpose(v, (1, 0, 2)))  # [H, P, hd]
+    for r0 in range(0, M, rows_per_block):
+        r1 = min(M, r0 + rows_per_block)
+        vis = visible[r0:r1]
+        cols = np.nonzero(vis.any(axis=0))[0]
+        if cols.size == 0:
+            continue
+        p_end = int(cols[-1]) + 1
+        qh = np.ascontiguousarray(np.transpose(q[r0:r1], (1, 0, 2)))  # [H, m, hd]
+        s = np.matmul(qh, kh[:, :, :p_end])
+        s /= np.sqrt(hd)
+        s += np.where(vis[:, :p_end], 0.0, -np.inf).astype(s.dtype)[None, :, :]
+        s -= np.max(s, axis=-1, keepdims=True)
+        np.exp(s, out=s)
+        s /= np.sum(s, axis=-1, keepdims=True)
+        out[r0:r1] = np.transpose(np.matmul(s, vh[:, :p_end]), (1, 0, 2))
+    return out
 
 
 def argmax_lowest(z: np.ndarray) -> int:

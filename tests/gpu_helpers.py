@@ -82,9 +82,14 @@ def check_step(art, b: int, dec: oracle.Decoder, t: float, ties: TieLog, forced=
             for u in dec.drafted[k]:
                 compare_lists(art["lists"][b, u, : dec.s[k]], lists_o[u], dz[u], t, ties, ff)
     elif dec.K:
+        # every tree token is the oracle's assembly (Sec. 4.4) of the GPU's own
+        # per-head lists: node (r_0..r_k) holds rank r_k of head k
+        lists_g = [[int(x) for x in art["lists"][b, k, : dec.s[k]]] for k in range(dec.K)]
+        want = dec.assemble(lists_g)
+        assert [int(x) for x in tree_g] == want, "tree tokens are not the assembly of the drafted lists"
         # the oracle's draft chain follows the GPU's rank-0 tokens (each checked
         # against the oracle's own list below, with the tie rule)
-        lists_o, dz = dec.draft(chain_tokens=[int(art["lists"][b, k, 0]) for k in range(dec.K)])
+        lists_o, dz = dec.draft(chain_tokens=[lst[0] for lst in lists_g])
         for k in range(dec.K):
             ff = forced is not None and bool(forced.ok[dec.n + 1 + k])
             compare_lists(art["lists"][b, k, : dec.s[k]], lists_o[k], dz[k], t, ties, ff)
@@ -187,3 +192,109 @@ def forced_lossless_run(cfg, weights, wl, steps: int, extra: int = 128, branch: 
     mean = total / (steps * B)
     log(f"{wl.name}: lossless over {B} x {steps} steps, mean accepted {mean:.2f}")
     return mean
+
+
+class GreedyRef:
+    """The oracle's own greedy stream from a decoder's state after prefill,
+    extended on demand one token per step through a root-only tree (the
+    decoder itself is left untouched).  tokens[i] is the token at absolute
+    position n0 + i, tokens[0] the pending token."""
+
+    def __init__(self, dec: oracle.Decoder):
+        self.ar = oracle.Decoder(dec.o, ())
+        for name in ("seq", "kv", "n", "pending", "h_last", "llm_k", "llm_v", "tri_k", "tri_v"):
+            setattr(self.ar, name, getattr(dec, name))
+        self.n0 = dec.n
+        self.tokens = [int(dec.pending)]
+
+    def upto(self, pos: int):
+        """Extend the stream to cover absolute position pos."""
+        while self.n0 + len(self.tokens) <= pos:
+            self.tokens += [int(x) for x in self.ar.step()["new_tokens"]]
+        return self.tokens
+
+
+def oracle_greedy_ref(dec: oracle.Decoder, n_tokens: int):
+    """The pending token and the n_tokens - 1 greedy tokens after it."""
+    r = GreedyRef(dec)
+    return r.upto(dec.n + n_tokens - 1)[:n_tokens]
+
+
+def teacher_forced_config(cfg, w_gpu, prompts, tree, accept_p, steps: int, *, compute=np.float32,
+                          page_size: int = 16, trigram_entries: int = 0, force_seed: int = 3,
+                          label: str = "", cache_weights: bool = True, orc=None):
+    """Teacher-forced node-by-node parity of `steps` GPU steps at a workload's
+    shape (batch = len(prompts)).
+
+    Forcing (the synthetic stand-in for a trained draft) biases both sides
+    toward the oracle's own greedy stream with per-sequence success
+    probabilities accept_p[b]; the same tables go to the GPU and to the
+    oracle.  Every step checks, per sequence: the drafted lists (tie rule),
+    the tree tokens as the assembly of those lists, the verify logits within
+    tau of the oracle's, the argmax per node (tie rule), the accepted path,
+    the committed tokens and the bonus.  Returns (max logit error, ties,
+    accepted lengths).  ``orc`` reuses an oracle already holding these weights."""
+    import torch
+    t = tau(cfg)
+    B = len(prompts)
+    K = max(len(r) for r in tree)
+    max_len = max(len(p) for p in prompts) + steps * (K + 1) + K + 2 + 64
+    max_len = (max_len + 63) // 64 * 64
+    stride = max_len + 8
+    if orc is None:
+        orc = oracle.Oracle(cfg, synth.weights_to_numpy(w_gpu), compute=compute, cache_weights=cache_weights)
+    log(f"{label}: oracle ({np.dtype(orc.ct).name}) prefill of {B} prompt(s) {[len(p) for p in prompts]}")
+    ref = np.full((B, stride), -1, dtype=np.int32)
+    ok = np.zeros((B, stride), dtype=np.uint8)
+    decs, grefs = [], []
+    for b, p in enumerate(prompts):
+        d = oracle.Decoder(orc, tree)
+        d.prefill([int(x) for x in p])
+        ok[b] = synth.force_table(float(accept_p[b]), force_seed, b, stride)
+        d.forcing = oracle.Forcing(ref[b], ok[b])  # views: later reference tokens show up here
+        decs.append(d)
+        grefs.append(GreedyRef(d))
+        log(f"{label}: sequence {b}: oracle prefill done")
+    sess = make_session(cfg, w_gpu, tree, max_batch=B, max_len=max_len)
+    if page_size != 16:
+        raise ValueError("sessions here use 16-token pages")
+    if trigram_entries:
+        sess.trigram_cache(trigram_entries)
+    ref_dev, ok_dev = torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda()
+    sess.set_forcing(ref_dev, ok_dev)
+    first = sess.prefill([np.asarray(p, dtype=np.int32) for p in prompts])
+    ties = TieLog()
+    for b, d in enumerate(decs):
+        if int(first[b]) != d.pending:  # admissible only as a tie of the oracle's own logits
+            logits, _, _ = d.o.causal_forward(d.seq[: d.n])
+            z = logits[-1]
+            assert abs(z[int(first[b])] - z[d.pending]) <= 2 * t * (z.max() - z.min())
+            d.pending = int(first[b])
+            d.seq[-1] = int(first[b])
+            ties.argmax_ties += 1
+
+    def extend_reference():
+        # a step with committed length n reads the forcing at n+1 .. n+K
+        for b, d in enumerate(decs):
+            g = grefs[b].upto(d.n + K + 1)
+            n0 = grefs[b].n0
+            ref[b, n0:n0 + len(g)] = g
+            ref_dev[b, n0:n0 + len(g)] = torch.from_numpy(ref[b, n0:n0 + len(g)].copy())
+        torch.cuda.synchronize()
+
+    errs, lens = [], []
+    for i in range(steps):
+        extend_reference()
+        art = gpu_step(sess)
+        for b, d in enumerate(decs):
+            new, err = check_step(art, b, d, t, ties, forced=d.forcing)
+            errs.append(err)
+            lens.append(len(new))
+        log(f"{label}: step {i}: max verify rel err {max(errs[-B:]):.2e}, accepted {lens[-B:]}")
+    if trigram_entries:
+        lookups, hits = sess.trigram_stats()
+        log(f"{label}: trigram cache {hits}/{lookups} hits")
+    sess.close()
+    log(f"{label}: {steps} steps x {B} sequence(s) match the oracle; max err {max(errs):.2e}, "
+        f"ties argmax {ties.argmax_ties}, lists {ties.list_ties}, mean accepted {np.mean(lens):.2f}")
+    return max(errs), ties, lens

@@ -2,25 +2,26 @@
 V 32000, bf16, 4 draft heads, 64-node tree) in the launch configuration the
 benchmark times.
 
-* Sampled outputs the oracle can compute: teacher-forced steps after a
-  130-token prompt (the shared MFMA attention pass over two chunks, a
-  partly masked one, and the 16-position window), checked
-  node by node against a float64 oracle holding every 7B weight.
-* Properties that hold at any size, on the benchmark workload itself
-  (512-token prompt, forced acceptance p = 0.7), on the 4096-token paged
-  context and on the ragged batch of 8 (prompts U[256, 2048], T32,
-  p_b ~ U[0.4, 0.9]): the speculative stream equals the GPU's greedy stream
-  token for token, and every step accepts exactly 1 + (consecutive seeded
-  successes) tokens along the rank-0 chain.
-* Branch-conditioned drafting: the teacher-forced check of every drafted
-  node's list, and the lossless forced run on the benchmark workload.
+* The benchmark workload itself, checked node by node: the 512-token
+  prompt, the 64-node tree and forced acceptance p = 0.7, for 8
+  teacher-forced steps against a float64 oracle holding every 7B weight
+  (drafted lists, tree assembly, verify logits, argmax, path, committed
+  tokens and bonus).
+* Branch-conditioned drafting: two teacher-forced steps after a 130-token
+  prompt with every drafted node's list checked.
+* Properties that hold at any size, on the benchmark workload, on the
+  4096-token paged context and on the ragged batch of 8 (prompts
+  U[256, 2048], T32, p_b ~ U[0.4, 0.9]): the speculative stream equals the
+  GPU's greedy stream token for token, and every step accepts exactly
+  1 + (consecutive seeded successes) tokens along the rank-0 chain.
 """
 import numpy as np
 import pytest
 
 import oracle
 import synth
-from gpu_helpers import TieLog, check_step, forced_lossless_run, gpu_step, log, make_session, tau
+from gpu_helpers import (TieLog, check_step, forced_lossless_run, gpu_step, log, make_session, tau,
+                         teacher_forced_config)
 
 pytestmark = pytest.mark.gpu
 
@@ -35,13 +36,21 @@ def w7b():
 
 @pytest.fixture(scope="module")
 def orc7b(w7b):
-    return oracle.Oracle(CFG, synth.weights_to_numpy(w7b), compute=np.float64, cache_weights=False)
+    log("llama7b: float64 oracle weights")
+    return oracle.Oracle(CFG, synth.weights_to_numpy(w7b), compute=np.float64)
 
 
-@pytest.mark.parametrize("branch", [False, True], ids=["chain", "branch"])
-def test_llama7b_teacher_forced_vs_oracle(w7b, orc7b, branch):
-    mode = "branch-conditioned" if branch else "chain"
-    log(f"llama7b: prompt 130, T64, {mode} drafting, 2 teacher-forced steps vs float64 oracle")
+def test_llama7b_p512_teacher_forced_vs_float64_oracle(w7b, orc7b):
+    wl = synth.WORKLOADS["llama7b_p512"]
+    err, ties, lens = teacher_forced_config(CFG, w7b, wl.prompts(), synth.TREE_T64, wl.accept_probs(), 8,
+                                            label="llama7b_p512", orc=orc7b)
+    assert err <= tau(CFG)
+    assert max(lens) > 1
+
+
+def test_llama7b_branch_teacher_forced_vs_oracle(w7b, orc7b):
+    branch = True
+    log("llama7b: prompt 130, T64, branch-conditioned drafting, 2 teacher-forced steps vs float64 oracle")
     prompt = synth.make_prompt(130, CFG.vocab, 41)
     sess = make_session(CFG, w7b, synth.TREE_T64, max_len=256)
     sess.set_drafting(branch)
