@@ -247,11 +247,34 @@ chimera_status chimera_set_trigram_cache(chimera_ctx* ctx, void* arena, int64_t 
 /* Cumulative draft-level trigram lookups and hits since the cache was attached. */
 chimera_status chimera_trigram_cache_stats(chimera_ctx* ctx, int64_t* lookups, int64_t* hits);
 
-/* Test hook: y[M][N] (float32, host) = x[M][K] @ w[K][N] through the
- * repack and GEMM kernels of `dtype`, on device buffers the call allocates
- * and frees itself.  x and w are host arrays of that dtype. */
+/* TEST HOOK -- allocates.  y[M][N] (float32, host) = x[M][K] @ w[K][N]
+ * through the repack and GEMM kernels of `dtype`, on device buffers the call
+ * allocates (hipMalloc) and frees itself; synchronises the device.  x and w
+ * are host arrays of that dtype.  M in [1, 256], N % 64 == 0, K a multiple
+ * of 32 (bf16) or 16 (f32); CHIMERA_EINVAL otherwise. */
 chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
                                   float* y);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * product as chimera_debug_gemm with every buffer in device memory and no
+ * allocation, no free and no synchronisation.
+ *   x: device [M][K] row-major, w: device [K][N] row-major, both of `dtype`
+ *   (caller-owned, only read); y: device float32 [M][N] row-major
+ *   (caller-owned, written); stream: hipStream_t or NULL.
+ * The call only enqueues its kernels on `stream`.  Its scratch -- the tiled
+ * copy of x, the repacked copy of w and the split-K partials -- is a 32 MiB
+ * static device array that every device holds until the process ends:
+ *   round256(mcap(M) K es) + round256(K N es) + splits M N 4 <= 32 MiB,
+ * with es the dtype size, mcap(M) M rounded up to 16, 32, 64 or a multiple
+ * of 128, and splits the reduction split the library picks for (N, K)
+ * (at most 8).  Larger shapes return CHIMERA_ENOMEM before any launch; the
+ * shape rules of chimera_debug_gemm give CHIMERA_EINVAL.  Every call on a
+ * device shares that device's scratch: calls that overlap on one device
+ * (other streams, other threads) race and must be serialised by the
+ * caller. */
+chimera_status chimera_gemm_static(int32_t dtype, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
+                                   float* y, void* stream);
 
 const char* chimera_last_error(void);
 void chimera_ctx_free(chimera_ctx* ctx);

@@ -66,6 +66,7 @@ _PROTOS = {
     "chimera_set_graph": [P, I32],
     "chimera_profile_read": [P, ctypes.POINTER(chimera_profile)],
     "chimera_debug_gemm": [I32, P, P, I32, I32, I32, ctypes.POINTER(ctypes.c_float)],
+    "chimera_gemm_static": [I32, P, P, I32, I32, I32, P, P],
     "chimera_trigram_cache_bytes": [P, I32, PI64],
     "chimera_set_decoding": [P, I32, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_uint64],
     "chimera_set_drafting": [P, I32],
@@ -190,6 +191,10 @@ def chimera_profile_read(ctx: int) -> chimera_profile:
 
 def chimera_debug_gemm(dtype: int, x_ptr: int, w_ptr: int, M: int, N: int, K: int, y_ptr: int):
     _check(lib().chimera_debug_gemm(dtype, x_ptr, w_ptr, M, N, K, ctypes.cast(y_ptr, ctypes.POINTER(ctypes.c_float))))
+
+
+def chimera_gemm_static(dtype: int, x_ptr: int, w_ptr: int, M: int, N: int, K: int, y_ptr: int, stream: int):
+    _check(lib().chimera_gemm_static(dtype, x_ptr, w_ptr, M, N, K, y_ptr, stream))
 
 
 def chimera_set_drafting(ctx: int, mode: int):

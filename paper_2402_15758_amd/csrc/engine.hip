@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <stdexcept>
 #include <string>
 #include <vector>
@@ -1466,6 +1467,84 @@ chimera_status chimera_debug_gemm(int32_t dtype, const void* x, const void* w, i
       throw;
     }
     cleanup();
+  });
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// GEMM with static scratch (chimera_gemm_static): the tiled copy of x, the
+// packed copy of w and the split-K partials live in this file-scope device
+// array instead of buffers the call allocates.  Each device holds its own
+// copy until the process ends; host code uses its per-device address from
+// hipGetSymbolAddress, never the array's name.
+// ---------------------------------------------------------------------------
+constexpr size_t GEMM_STATIC_SCRATCH_BYTES = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[GEMM_STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+// Device address of `scratch` on the current device, looked up once per device.
+char* static_scratch() {
+  int dev = -1;
+  HIPCK(hipGetDevice(&dev));
+  REQUIRE(dev >= 0 && dev < MAX_DEVICES, CHIMERA_EINVAL, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    HIPCK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    REQUIRE(p != nullptr, CHIMERA_EHIP, "no device address for the static scratch");
+    g_scratch_ptr[dev] = p;
+  }
+  return (char*)g_scratch_ptr[dev];
+}
+
+size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+}  // namespace
+
+extern "C" {
+
+chimera_status chimera_gemm_static(int32_t dtype, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
+                                   float* y, void* stream) {
+  return guard([&] {
+    REQUIRE(dtype == CHIMERA_F32 || dtype == CHIMERA_BF16, CHIMERA_EINVAL, "dtype");
+    REQUIRE(x && w && y, CHIMERA_EINVAL, "null argument");
+    const int KB = dtype == CHIMERA_BF16 ? 32 : 16;
+    REQUIRE(M >= 1 && M <= 256 && N % 64 == 0 && N > 0 && K % KB == 0 && K > 0, CHIMERA_EINVAL,
+            "M in [1, 256], N % 64 == 0, K % KB == 0");
+    const size_t es = esize(dtype);
+    const int mc = mcap(M);
+    const int splits = gemm_pick_splits(N, K, dtype);
+    const size_t xb = round256((size_t)mc * K * es);
+    const size_t wb = round256((size_t)K * N * es);
+    const size_t pb = splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
+    REQUIRE(xb + wb + pb <= GEMM_STATIC_SCRATCH_BYTES, CHIMERA_ENOMEM,
+            "tiled x + packed w + split-K partials exceed the 32 MiB static scratch (" +
+                std::to_string(xb + wb + pb) + " bytes)");
+    hipStream_t st = (hipStream_t)stream;
+    char* base = static_scratch();
+    // Rows of the last 16-row tile past M keep an earlier call's values; each
+    // output row depends only on its own input row and rows >= M are not stored.
+    launch_tile_rows(dtype, x, M, K, base, mc / 16, st);
+    launch_repack(dtype, PACK_NATURAL, w, nullptr, nullptr, K, N, base + xb, 1, 64, st);
+    GemmShape s;
+    s.X = base;
+    s.x_mtiles = mc / 16;
+    s.M = M;
+    s.W = base + xb;
+    s.N = N;
+    s.K = K;
+    s.splits = splits;
+    GemmEpi e;
+    e.kind = EPI_F32;
+    e.out_f = y;
+    e.ldo = N;
+    e.part = (float*)(base + xb + wb);
+    launch_gemm(dtype, s, e, st);
+    HIPCK(hipGetLastError());
   });
 }
 
