@@ -9,16 +9,25 @@ The default workload is the Llama-7B-shaped bf16 model (random N(0, 0.02)
 weights), batch 1, a uniform random 512-token prompt, the 64-node tree and
 forced acceptance p = 0.7 (the paper's datasets and trained drafts are
 replaced by synthetic prompts and a seeded acceptance bias).  W untimed
-steps run first, then exactly K steps are timed; the line printed is
+steps run first, then exactly K steps are timed (HIP graph replay, the
+launch mode of the library); the line printed is
 
   value = accepted (committed) tokens / timed seconds.
 
-Also reported: the verify GEMM kernel's achieved HBM bandwidth from HIP
-events around each of its launches in the timed steps (roofline), the whole
-verify pass's fraction of HBM peak, the plain greedy decoding rate of the
-same GPU path (tree of one node), the CPU oracle on a bounded sample, and
-side measurements of the trigram lookup cache, branch-conditioned drafting
-and typical decoding.
+Also reported:
+  verify_pass  the verify pass (tree pass + LM head + argmax) timed by device
+               wall-clock stamps inside the replayed step graph, median over
+               K steps, against its algorithmic bytes (weights + KV read +
+               tree KV write) and against HBM peak and a measured device copy;
+  roofline     the verify GEMM kernels' achieved HBM bandwidth, from HIP
+               events recorded by each launch's own dispatch (K steps with the
+               kernels launched one by one);
+  generation   the workload's whole generation (G tokens after the prefill),
+               timed three times, median tokens/s;
+  cpu_baseline the CPU oracle's own decode steps on this host, timed;
+and the plain greedy decoding rate of the same GPU path (tree of one node),
+plus side measurements of the trigram lookup cache, branch-conditioned
+drafting and typical decoding.
 """
 from __future__ import annotations
 
@@ -79,51 +88,61 @@ def drafted_per_level(tree):
     return [sum(1 for r in internal if len(r) == k) for k in range(K)]
 
 
-def cpu_baseline(wl, weights_gpu, prompt, accept_len):
-    """The oracle on a bounded sample of the workload: one decode step of
-    the full draft and of the first two target layers plus the LM head,
-    after a prefill of the same prompt; the target part is scaled to all
-    layers.  Reported in accepted tokens/s with the realised mean accepted
-    length of the GPU run."""
-    import dataclasses
-
+def cpu_baseline(wl, weights_gpu, prompt, ref_row, ok_row, n_steps=8):
+    """The CPU oracle on a bounded sample of the workload: after an untimed
+    prefill of the same prompt and one untimed step (which also converts the
+    draft weights), n_steps of its own decode steps (draft, tree verify over
+    every target layer, acceptance and commit) with the same forced-acceptance
+    tables as the GPU run, timed.  Reported in accepted tokens/s."""
     import oracle
     import synth
     cfg = wl.model
-    n_sample = 2
-    sub = dataclasses.replace(cfg, n_layers=n_sample)
-    keep = [n for n, _, _ in synth.tensor_specs(sub)]
-    w = synth.weights_to_numpy({k: weights_gpu[k] for k in keep})
     threads = len(os.sched_getaffinity(0))
     omp = os.environ.get("OMP_NUM_THREADS")
     if omp:
         threads = min(threads, int(omp))
-    orc = oracle.Oracle(sub, w, compute=np.float32)
-    dec = oracle.Decoder(orc, synth.TREES[wl.tree])
+    orc = oracle.Oracle(cfg, synth.weights_to_numpy(weights_gpu), compute=np.float32)
+    dec = oracle.Decoder(orc, synth.TREES[wl.tree], forcing=oracle.Forcing(ref_row, ok_row))
     t0 = time.perf_counter()
-    dec.prefill(list(prompt))
+    dec.prefill([int(x) for x in prompt])
     t_prefill = time.perf_counter() - t0
+    log(f"[bench] oracle prefill {t_prefill:.1f}s")
+    dec.step()
     t0 = time.perf_counter()
-    lists, _ = dec.draft()
-    t_draft = time.perf_counter() - t0
-    toks = dec.assemble(lists)
-    t0 = time.perf_counter()
-    logits, h, tkv = dec.verify(toks)
-    t_verify = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    _ = h @ orc.w("lm_head")
-    t_head = time.perf_counter() - t0
-    t_layers = max(t_verify - t_head, 0.0)
-    t_step = t_draft + t_layers * (cfg.n_layers / n_sample) + t_head
+    accepted = 0
+    for i in range(n_steps):
+        accepted += len(dec.step()["new_tokens"])
+        log(f"[bench] oracle step {i}: {time.perf_counter() - t0:.1f}s")
+    t_steps = time.perf_counter() - t0
     return {
-        "value": accept_len / t_step,
+        "value": accepted / t_steps,
         "unit": "tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"one float32 oracle step (draft + {n_sample} of {cfg.n_layers} target layers + LM head, "
-                   f"64-node tree, context {len(prompt)}), target layers scaled x{cfg.n_layers // n_sample}; "
-                   f"prefill {t_prefill:.1f}s excluded; step {t_step:.2f}s"),
+        "sample": (f"{n_steps} float32 oracle decode steps of the workload (all {cfg.n_layers} target layers, "
+                   f"draft, {wl.tree} tree, context {len(prompt)}+, same forcing), {accepted} tokens accepted in "
+                   f"{t_steps:.1f}s ({t_steps / n_steps:.2f} s/step); prefill {t_prefill:.1f}s and one warm-up "
+                   f"step not timed"),
     }
+
+
+def copy_bandwidth(torch, dev, nbytes=1 << 30, reps=5):
+    """Device-to-device copy of nbytes (read + write) timed with HIP events:
+    the streaming reference bandwidth of this GPU, in GB/s."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = None
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        e1.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    del src, dst
+    return 2.0 * nbytes / (best * 1e-3) / 1e9
 
 
 def counter_traffic():
@@ -146,6 +165,18 @@ def counter_traffic():
     return rec["traffic_bytes_per_launch"]
 
 
+def run_steps(spec, n, out):
+    """n steps; appends each sequence's committed tokens to out; returns the
+    accepted count."""
+    acc = 0
+    for _ in range(n):
+        toks, nn, _ = spec.step()
+        acc += int(nn.sum())
+        for b in range(len(out)):
+            out[b] += [int(x) for x in toks[b, : nn[b]]]
+    return acc
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -160,9 +191,11 @@ def main():
     wl = synth.WORKLOADS[a.workload]
     cfg = wl.model
     prompts = wl.prompts()
+    B = len(prompts)
     K_levels = max(len(r) for r in synth.TREES[wl.tree])
-    total_steps = a.warmup + 2 * a.steps  # warmup, timed pass, profiled pass
-    max_len = max(len(p) for p in prompts) + total_steps * (K_levels + 1) + 128
+    total_steps = a.warmup + 2 * a.steps  # warmup, timed pass, eager-profiled pass
+    horizon = max(total_steps * (K_levels + 1), wl.gen_tokens + K_levels + 1)
+    max_len = max(len(p) for p in prompts) + horizon + 128
     max_len = (max_len + 63) // 64 * 64
     torch.cuda.init()
     dev = torch.device("cuda:0")
@@ -171,60 +204,73 @@ def main():
     weights = synth.make_weights(cfg, wl.target_seed, wl.draft_seed, device="cuda")
     torch.cuda.synchronize()
     log(f"[bench] weights ready in {time.perf_counter() - t0:.1f}s; loading")
-    spec = Session(cfg, weights, synth.TREES[wl.tree], max_batch=len(prompts), max_len=max_len)
-    ar = Session(cfg, None, (), max_batch=len(prompts), max_len=max_len, share_model=spec)
+    spec = Session(cfg, weights, synth.TREES[wl.tree], max_batch=B, max_len=max_len)
+    ar = Session(cfg, None, (), max_batch=B, max_len=max_len, share_model=spec)
     torch.cuda.synchronize()
 
     # greedy reference stream (plain decoding through the same kernels)
-    n_ref = total_steps * (K_levels + 1) + K_levels + 2
+    n_ref = horizon + K_levels + 2
     log(f"[bench] greedy decoding {n_ref} tokens for the forcing reference")
     streams = [[int(t)] for t in ar.prefill(prompts)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     while min(len(s) for s in streams) < n_ref:
         toks, n, _ = ar.step()
-        for b in range(len(prompts)):
+        for b in range(B):
             streams[b] += [int(x) for x in toks[b, : n[b]]]
     torch.cuda.synchronize()
-    ar_rate = len(prompts) * (n_ref - 1) / (time.perf_counter() - t0)
+    ar_rate = B * (n_ref - 1) / (time.perf_counter() - t0)
     stride = max_len + 8
     ref, ok = forcing_tables(wl, prompts, streams, stride)
     spec.set_forcing(torch.from_numpy(ref).to(dev), torch.from_numpy(ok).to(dev))
 
     log(f"[bench] spec: prefill, {a.warmup} warmup steps, {a.steps} timed steps")
-    first = spec.prefill(prompts)
-    out = [[int(t)] for t in first]
-    for _ in range(a.warmup):
-        toks, n, _ = spec.step()
-        for b in range(len(prompts)):
-            out[b] += [int(x) for x in toks[b, : n[b]]]
-    # timed pass: exactly K steps, no per-kernel events
+    out = [[int(t)] for t in spec.prefill(prompts)]
+    run_steps(spec, a.warmup, out)
+    # timed pass: exactly K steps, graph replay.  Every step carries one-lane
+    # wall-clock stamp kernels at its phase boundaries (draft | verify | tail);
+    # the library reports the per-step medians of exactly these steps.
+    spec.profile_read()  # opens the stamp window
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    accepted = 0
-    for _ in range(a.steps):
-        toks, n, _ = spec.step()
-        accepted += int(n.sum())
-        for b in range(len(prompts)):
-            out[b] += [int(x) for x in toks[b, : n[b]]]
+    accepted = run_steps(spec, a.steps, out)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    # profiled pass: K more steps with HIP events on the stream the kernels
-    # run on: around each phase, and recorded by each verify GEMM kernel's
-    # own dispatch at its start and end (kernels launched one by one here)
+    prof_g = spec.profile_read()
+    # eager-profiled pass: kernels launched one by one, each verify GEMM
+    # launch recording HIP events at its own dispatch start and end
     spec.set_graph(False)
     spec.profile(True)
-    accepted_p = 0
-    for _ in range(a.steps):
-        toks, n, _ = spec.step()
-        accepted_p += int(n.sum())
-        for b in range(len(prompts)):
-            out[b] += [int(x) for x in toks[b, : n[b]]]
+    spec.profile_read()
+    run_steps(spec, a.steps, out)
     torch.cuda.synchronize()
     prof = spec.profile_read()
     spec.profile(False)
     spec.set_graph(True)
-    lossless = all(out[b] == streams[b][: len(out[b])] for b in range(len(prompts)))
+    lossless = all(out[b] == streams[b][: len(out[b])] for b in range(B))
+
+    # the whole generation: G tokens per sequence after the prefill, three times
+    gen = []
+    for rep in range(3):
+        o = [[int(t)] for t in spec.prefill(prompts)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        steps = 0
+        while min(len(x) for x in o) < wl.gen_tokens:
+            run_steps(spec, 1, o)
+            steps += 1
+        torch.cuda.synchronize()
+        t_gen = time.perf_counter() - t0
+        committed = sum(len(x) - 1 for x in o)
+        gen.append((committed / t_gen, steps, committed, t_gen))
+        lossless = lossless and all(o[b] == streams[b][: len(o[b])] for b in range(B))
+    gen_sorted = sorted(gen)
+    generation = {"tokens": wl.gen_tokens, "reps": 3,
+                  "tokens_per_s_median": round(gen_sorted[1][0], 2),
+                  "tokens_per_s": [round(g[0], 2) for g in gen],
+                  "steps": [g[1] for g in gen], "committed": [g[2] for g in gen],
+                  "timing": "first chimera_step to the last synchronisation, prefill excluded"}
+    log(f"[bench] generation of {wl.gen_tokens} tokens x3: {generation['tokens_per_s']} tok/s")
 
     tri = None
     if a.trigram_cache:
@@ -270,6 +316,7 @@ def main():
             toks, n, _ = spec.step()
             for b in range(len(prompts)):
                 out3[b] += [int(x) for x in toks[b, : n[b]]]
+        spec.profile_read()  # opens the stamp window
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         acc4 = 0
@@ -280,31 +327,25 @@ def main():
                 out3[b] += [int(x) for x in toks[b, : n[b]]]
         torch.cuda.synchronize()
         dt4 = time.perf_counter() - t0
-        spec.set_graph(False)
-        spec.profile(True)
-        for _ in range(a.steps):
-            toks, n, _ = spec.step()
-            for b in range(len(prompts)):
-                out3[b] += [int(x) for x in toks[b, : n[b]]]
-        torch.cuda.synchronize()
         pb = spec.profile_read()
-        spec.profile(False)
-        spec.set_graph(True)
         spec.set_drafting(False)
         same = all(out3[b] == out[b][: len(out3[b])] for b in range(len(prompts)))
         br = {"tokens_per_s": round(acc4 / dt4, 2), "ms_per_step": round(dt4 / a.steps * 1e3, 4),
-              "draft_ms": round(pb.ms_draft / pb.steps, 4), "chain_draft_ms": round(prof.ms_draft / prof.steps, 4),
+              "draft_ms": round(pb.ms_draft_median, 4), "chain_draft_ms": round(prof_g.ms_draft_median, 4),
               "queries_per_level": [len(prompts) * r for r in drafted_per_level(synth.TREES[wl.tree])],
               "same_stream": same}
         log(f"[bench] branch-conditioned drafting: {br}")
     value = accepted / dt
+    verify_bytes_step = prof_g.verify_bytes / max(prof_g.steps, 1)
+    verify_ms = prof_g.ms_verify_median
+    verify_gbs = verify_bytes_step / (verify_ms * 1e-3) / 1e9
     gemm_gbs = prof.gemm_verify_bytes / (prof.ms_gemm_verify * 1e-3) / 1e9
-    verify_gbs = prof.verify_bytes / (prof.ms_verify * 1e-3) / 1e9
     per_launch_bytes = prof.gemm_verify_bytes / max(prof.gemm_verify_launches, 1)
     per_launch_us = prof.ms_gemm_verify * 1e3 / max(prof.gemm_verify_launches, 1)
-    log(f"[bench] {value:.1f} tok/s, {dt / a.steps * 1e3:.3f} ms/step, accept {accepted / a.steps / len(prompts):.3f}, "
-        f"verify {prof.ms_verify / prof.steps:.3f} ms ({verify_gbs:.0f} GB/s), draft {prof.ms_draft / prof.steps:.3f} ms, "
-        f"gemm {gemm_gbs:.0f} GB/s, lossless={lossless}")
+    copy_gbs = copy_bandwidth(torch, dev)
+    log(f"[bench] {value:.1f} tok/s, {dt / a.steps * 1e3:.3f} ms/step, accept {accepted / a.steps / B:.3f}, "
+        f"verify {verify_ms:.3f} ms in the graph ({verify_gbs:.0f} GB/s), draft {prof_g.ms_draft_median:.3f} ms, "
+        f"gemm {gemm_gbs:.0f} GB/s, copy {copy_gbs:.0f} GB/s, lossless={lossless}")
 
     if a.calibrate_copy:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
@@ -315,12 +356,13 @@ def main():
         log("[bench] copy calibration: 3 x 1 GiB device copies")
         del src, dst
     cpu = None
-    if not a.no_cpu_baseline and len(prompts) == 1:
-        log("[bench] CPU oracle baseline (bounded sample)")
+    if not a.no_cpu_baseline and B == 1:
+        log("[bench] CPU oracle baseline (8 timed oracle steps)")
         try:
-            cpu = cpu_baseline(wl, weights, prompts[0], accepted / a.steps)
+            cpu = cpu_baseline(wl, weights, prompts[0], ref[0], ok[0])
         except MemoryError:
             cpu = None
+        log(f"[bench] CPU oracle: {cpu}")
     typ = None
     if not a.no_typical:
         # typical decoding at T = 1 (sampling, not lossless): accepted length and
@@ -371,10 +413,10 @@ def main():
             "workload": wl.name,
             "target": f"{cfg.n_layers}L d{cfg.d_model} {cfg.n_heads}x{cfg.head_dim} F{cfg.d_ffn} V{cfg.vocab}",
             "draft": f"trigram MLP + 1 encoder layer + {cfg.n_draft_heads} heads",
-            "batch": len(prompts),
-            "prompt_len": [len(p) for p in prompts] if len(prompts) > 1 else len(prompts[0]),
+            "batch": B,
+            "prompt_len": [len(p) for p in prompts] if B > 1 else len(prompts[0]),
             "tree": wl.tree,
-            "accept_p": wl.accept_p[0] if wl.accept_p and len(prompts) == 1 else wl.accept_p,
+            "accept_p": wl.accept_p[0] if wl.accept_p and B == 1 else wl.accept_p,
             "page_size": 16,
         },
         "roofline": {
@@ -387,16 +429,23 @@ def main():
             "traffic": (round(counter_traffic()) if counter_traffic() and wl.name == "llama7b_p512" else None),
             "bytes_per_launch": round(per_launch_bytes),
             "us_per_launch": round(per_launch_us, 2),
+            "launches_per_step": round(prof.gemm_verify_launches / max(prof.steps, 1), 2),
         },
         "verify_pass": {
-            "ms": round(prof.ms_verify / prof.steps, 4),
-            "bytes": round(prof.verify_bytes / prof.steps),
+            "ms": round(verify_ms, 4),
+            "ms_mean": round(prof_g.ms_verify / max(prof_g.steps, 1), 4),
+            "bytes": round(verify_bytes_step),
             "achieved_gbs": round(verify_gbs, 1),
             "frac_hbm_peak": round(verify_gbs / HBM_PEAK_GBS, 4),
+            "frac_copy_bw": round(verify_gbs / copy_gbs, 4),
+            "timing": "device wall-clock stamps around the verify pass inside the replayed step graph, median over the timed steps",
         },
-        "draft_ms": round(prof.ms_draft / prof.steps, 4),
-        "tail_ms": round(prof.ms_tail / prof.steps, 4),
-        "accept_len_mean": round(accepted / a.steps / len(prompts), 4),
+        "step_ms_stamped_median": round(prof_g.ms_step_median, 4),
+        "copy_bw_gbs": round(copy_gbs, 1),
+        "draft_ms": round(prof_g.ms_draft_median, 4),
+        "tail_ms": round(prof_g.ms_tail / max(prof_g.steps, 1), 4),
+        "accept_len_mean": round(accepted / a.steps / B, 4),
+        "generation": generation,
         "lossless_vs_greedy": lossless,
         "trigram_cache": tri,
         "typical_decoding": typ,

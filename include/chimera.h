@@ -79,7 +79,7 @@ typedef struct {
   const void* data;
   int64_t numel;
   int32_t dtype;     /* chimera_dtype */
-  int32_t on_device; /* 1: data is device memory, 0: host memory */
+  int32_t on_device; /* must be 1: data is device memory (host tensors give CHIMERA_EINVAL) */
 } chimera_tensor;
 
 /* Bytes of the weight arena for this config (repacked weights + rotary
@@ -88,8 +88,9 @@ chimera_status chimera_weight_bytes(const chimera_config* cfg, int64_t* bytes);
 
 /* Validate the tensor list and repack every tensor into `arena` (device
  * memory of at least chimera_weight_bytes) in the order the GEMM kernels
- * stream it.  Reads the caller's tensors once; they may be freed after the
- * call returns.  Synchronises `stream`. */
+ * stream it.  Every tensor must already be in device memory; the call reads
+ * each once, allocates nothing, and the caller may free them after it
+ * returns.  Synchronises `stream`. */
 chimera_status chimera_load(const chimera_config* cfg, const chimera_tensor* tensors, int32_t n_tensors,
                             void* arena, int64_t arena_bytes, void* stream, chimera_model** out);
 
@@ -165,23 +166,33 @@ chimera_status chimera_debug_copy(chimera_ctx* ctx, int32_t what, void* dst, int
 chimera_status chimera_kv_read(chimera_kv* kv, int32_t layer, int32_t b, int32_t pos0, int32_t count, void* k_out,
                                void* v_out);
 
-/* Per-phase timing of steps, recorded with HIP events on the step's stream
- * while enabled: draft, verify (tree pass + LM head), tail (accept, compact,
- * advance) and the verify-pass GEMM launches alone. */
+/* Per-phase timing of steps.  Phases: draft, verify (tree pass + LM head +
+ * argmax), tail (accept, compact, advance).  Every step (graph replay or
+ * eager launches) runs a one-lane kernel at each phase boundary that
+ * records the device wall clock into a ring of the last 4096 steps, so a
+ * replayed graph is timed as it runs.  chimera_profile_read synchronises the
+ * device and reports the steps stamped since its previous call (or since
+ * the context was created; at most the last 4096), then starts a new window.
+ * chimera_profile_enable(ctx, 1) only adds per-launch HIP events to every
+ * verify-pass GEMM launched eagerly (chimera_set_graph(ctx, 0)): the
+ * ms_gemm_verify, gemm_verify_launches and gemm_verify_bytes fields, summed
+ * since the previous read (zero under graph replay). */
 typedef struct {
   int64_t steps;
-  double ms_draft, ms_verify, ms_tail, ms_gemm_verify;
+  double ms_draft, ms_verify, ms_tail, ms_gemm_verify;  /* sums over the steps */
   int64_t gemm_verify_launches;
   double gemm_verify_bytes; /* algorithmic bytes of those launches: weights + activations in/out */
   double verify_bytes;      /* algorithmic bytes of the verify passes: weights, KV read and write */
+  double ms_draft_median, ms_verify_median, ms_step_median; /* per-step medians (step: first to last stamp) */
 } chimera_profile;
 chimera_status chimera_profile_enable(chimera_ctx* ctx, int32_t enable);
 chimera_status chimera_profile_read(chimera_ctx* ctx, chimera_profile* out);
 
 /* Launch mode of chimera_step: 1 (default) captures the step's launch
  * sequence once into a HIP graph and replays it every step (recaptured after
- * prefill, set_forcing, profile_enable or a stream change; needs a non-null
- * stream); 0 launches every kernel individually.  Results are identical. */
+ * prefill, set_forcing, set_drafting, set_decoding, set_trigram_cache or a
+ * stream change; needs a non-null stream); 0 launches every kernel
+ * individually.  Results are identical. */
 chimera_status chimera_set_graph(chimera_ctx* ctx, int32_t enable);
 
 /* Verification rule (Sec. 4.3; Sec. 5.1 tests greedy and typical decoding at

@@ -39,7 +39,8 @@ class chimera_profile(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int64), ("ms_draft", ctypes.c_double), ("ms_verify", ctypes.c_double),
                 ("ms_tail", ctypes.c_double), ("ms_gemm_verify", ctypes.c_double),
                 ("gemm_verify_launches", ctypes.c_int64), ("gemm_verify_bytes", ctypes.c_double),
-                ("verify_bytes", ctypes.c_double)]
+                ("verify_bytes", ctypes.c_double), ("ms_draft_median", ctypes.c_double),
+                ("ms_verify_median", ctypes.c_double), ("ms_step_median", ctypes.c_double)]
 
 
 _lib = None

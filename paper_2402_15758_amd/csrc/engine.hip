@@ -231,20 +231,28 @@ struct chimera_ctx {
   const int* f_ref = nullptr;
   const uint8_t* f_ok = nullptr;
   int f_stride = 0;
-  int* host_out = nullptr;  // pinned [3][B][K+1]
+  // Step results, one contiguous device block copied back by one transfer:
+  // out_tok [B][K+1], out_nodes [B][K+1], out_len [B] (K = the depth the
+  // context was sized for).
+  char* result = nullptr;
+  char* host_result = nullptr;  // pinned mirror
+  size_t res_bytes = 0, res_nodes_off = 0, res_len_off = 0;
   // profiling
   bool prof = false;
   std::vector<Event2> ev_pool;
   size_t ev_used = 0;
   std::vector<double> ev_bytes;
-  hipEvent_t e_start{}, e_draft{}, e_verify{}, e_end{};
+  unsigned long long* stamp_ring = nullptr;  // device [STAMP_RING][STAMP_WORDS], one slot per step
+  unsigned int* stamp_count = nullptr;       // device: steps stamped so far
+  unsigned int prof_first = 0;               // stamp_count at the previous chimera_profile_read
+  double clock_khz = 0.0;
   bool ev_created = false;
   chimera_profile acc{};
   // the step as a HIP graph, replayed every step
   bool graph_on = true;
   hipGraph_t graph = nullptr;
   hipGraphExec_t gexec = nullptr;
-  bool graph_prof = false;
+  bool capturing = false;  // chimera_step is capturing its launch sequence
   hipStream_t graph_stream = nullptr;
   size_t graph_ev_used = 0;
 };
@@ -315,22 +323,19 @@ struct Gemm {
     REQUIRE(tiles_read <= x_mtiles, CHIMERA_EINVAL, "GEMM rows exceed the input buffer");
     if (e.kind != EPI_PARTIAL) e.part = c->scratch;
     Event2* ev = nullptr;
-    if (timed && c->prof && c->ev_used < c->ev_pool.size()) {
+    // per-launch events only for eager launches; a captured graph keeps the
+    // phase stamps alone (querying the capture state for every launch while
+    // capturing made the replayed graph slower)
+    if (timed && c->prof && !c->capturing && c->ev_created && c->ev_used < c->ev_pool.size()) {
       ev = &c->ev_pool[c->ev_used];
       const double es = (double)c->m->es;
       c->ev_bytes[c->ev_used] = (double)K * cols * es + (double)M * K * es + (double)M * cols * 4.0;
       c->ev_used++;
     }
-    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    if (ev) HIPCK(hipStreamIsCapturing(st, &cap));
-    if (ev && cap == hipStreamCaptureStatusNone) {
-      // launched kernels record the events at their own start and end
+    if (ev)  // the kernels record the events at their own start and end
       launch_gemm(c->m->dt, s, e, st, ev->a, ev->b);
-    } else {
-      if (ev) HIPCK(hipEventRecord(ev->a, st));
+    else
       launch_gemm(c->m->dt, s, e, st);
-      if (ev) HIPCK(hipEventRecord(ev->b, st));
-    }
   }
   int splits(int N, int K) const { return gemm_pick_splits(N, K, c->m->dt); }
 };
@@ -636,9 +641,17 @@ void carve_ctx(chimera_ctx* c, Arena& a) {
   c->inject = a.arr<int>(B * std::max<size_t>(N, 2));
   c->inject_on = a.arr<int>(1);
   c->s_k_dev = a.arr<int>(8);
-  c->out_tok = a.arr<int>(B * (K + 1));
-  c->out_nodes = a.arr<int>(B * (K + 1));
-  c->out_len = a.arr<int>(B);
+  c->res_nodes_off = sizeof(int) * B * (K + 1);
+  c->res_len_off = 2 * c->res_nodes_off;
+  c->res_bytes = c->res_len_off + sizeof(int) * B;
+  c->result = (char*)a.take(c->res_bytes);
+  if (c->result != nullptr) {
+    c->out_tok = (int*)c->result;
+    c->out_nodes = (int*)(c->result + c->res_nodes_off);
+    c->out_len = (int*)(c->result + c->res_len_off);
+  }
+  c->stamp_ring = a.arr<unsigned long long>((size_t)STAMP_RING * STAMP_WORDS);
+  c->stamp_count = a.arr<unsigned int>(1);
   c->pro_base = a.arr<int>(B);
   c->pro_count = a.arr<int>(B);
   c->pro_h = a.take(B * (K + 1) * d * es);
@@ -774,16 +787,17 @@ void ctx_dims(chimera_ctx* c) {
   c->nblk_enc = (2 * c->kv->cap + cf.n_draft_heads + 1 + 255) / 256;
 }
 
-void prof_bytes_verify(chimera_ctx* c) {
+// Algorithmic bytes of one verify pass: every target weight once (norm
+// gains included), the KV read over the committed lengths (sum_n summed over
+// the batch) and the tree's own K/V rows written.
+double verify_pass_bytes(const chimera_ctx* c, double sum_n) {
   const chimera_model* m = c->m;
   const chimera_config& cf = m->cfg;
   const double es = (double)m->es, d = cf.d_model, F = cf.d_ffn, V = cf.vocab;
   const double hdim = (double)cf.n_heads * cf.head_dim;
   const double w_layer = (d * 3 * hdim + hdim * d + d * 2 * F + F * d) * es + 2 * d * 4;
-  double bytes = cf.n_layers * w_layer + d * V * es + d * 4;
-  for (int b = 0; b < c->batch; ++b)
-    bytes += (double)cf.n_layers * 2 * hdim * es * ((double)c->n_host[b] + c->N);
-  c->acc.verify_bytes += bytes;
+  const double bytes = cf.n_layers * w_layer + d * V * es + d * 4;
+  return bytes + (double)cf.n_layers * 2 * hdim * es * (sum_n + (double)c->batch * c->N);
 }
 
 }  // namespace
@@ -849,6 +863,8 @@ chimera_status chimera_load(const chimera_config* cfg, const chimera_tensor* ten
       REQUIRE(it != want.end(), CHIMERA_EINVAL, std::string("unexpected tensor ") + t.name);
       REQUIRE(t.numel == it->second.first, CHIMERA_EINVAL, std::string("wrong size for ") + t.name);
       REQUIRE(t.dtype == it->second.second, CHIMERA_EINVAL, std::string("wrong dtype for ") + t.name);
+      REQUIRE(t.on_device == 1, CHIMERA_EINVAL,
+              std::string("tensor ") + t.name + " is not in device memory (copy it to the device first)");
       have[t.name] = &t;
     }
     for (auto& kvp : want) REQUIRE(have.count(kvp.first), CHIMERA_EINVAL, "missing tensor " + kvp.first);
@@ -868,21 +884,11 @@ chimera_status chimera_load(const chimera_config* cfg, const chimera_tensor* ten
       m->es = es;
       Arena a{(char*)arena, (size_t)arena_bytes};
       carve_model(c, a, *m);
-      std::vector<void*> staging;
-      auto dev = [&](const std::string& name) -> const void* {
-        const chimera_tensor* t = have[name];
-        const size_t bytes = (size_t)t->numel * (t->dtype == CHIMERA_F32 ? 4 : 2);
-        if (t->on_device) return t->data;
-        void* p = nullptr;
-        HIPCK(hipMalloc(&p, bytes));
-        staging.push_back(p);
-        HIPCK(hipMemcpy(p, t->data, bytes, hipMemcpyHostToDevice));
-        return p;
-      };
+      auto dev = [&](const std::string& name) -> const void* { return have[name]->data; };
       auto copy = [&](void* dst, const std::string& name) {
         const chimera_tensor* t = have[name];
         const size_t bytes = (size_t)t->numel * (t->dtype == CHIMERA_F32 ? 4 : 2);
-        HIPCK(hipMemcpyAsync(dst, t->data, bytes, t->on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, st));
+        HIPCK(hipMemcpyAsync(dst, t->data, bytes, hipMemcpyDeviceToDevice, st));
       };
       auto pack = [&](void* dst, int kind, const std::string& a0, const std::string& a1, const std::string& a2, int K,
                       int n_src) {
@@ -901,12 +907,7 @@ chimera_status chimera_load(const chimera_config* cfg, const chimera_tensor* ten
         pack(w.wdown, PACK_NATURAL, p + "w_down", "", "", (int)F, (int)d);
       };
       copy(m->embed, "tok_embed");
-      for (int l = 0; l < c.n_layers; ++l) {
-        block("layers." + std::to_string(l) + ".", m->layers[l]);
-        HIPCK(hipStreamSynchronize(st));
-        for (void* p : staging) HIPCK(hipFree(p));
-        staging.clear();
-      }
+      for (int l = 0; l < c.n_layers; ++l) block("layers." + std::to_string(l) + ".", m->layers[l]);
       copy(m->final_norm, "final_norm");
       pack(m->lm_head, PACK_NATURAL, "lm_head", "", "", (int)d, (int)V);
       pack(m->tri_w1, PACK_NATURAL, "draft.tri_w1", "", "", (int)(3 * d), (int)d);
@@ -930,7 +931,6 @@ chimera_status chimera_load(const chimera_config* cfg, const chimera_tensor* ten
       HIPCK(hipMemcpyAsync(m->rcos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, st));
       HIPCK(hipMemcpyAsync(m->rsin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, st));
       HIPCK(hipStreamSynchronize(st));
-      for (void* p : staging) HIPCK(hipFree(p));
     } catch (...) {
       delete m;
       throw;
@@ -1100,11 +1100,12 @@ chimera_status chimera_ctx_create(chimera_model* m, chimera_kv* kv, const int32_
       HIPCK(hipMemset(c->tri.miss, 0, sizeof(int)));
       HIPCK(hipMemset(c->tri.stats, 0, 2 * sizeof(unsigned long long)));
       HIPCK(hipMemset(c->n, 0, sizeof(int) * c->B));
+      HIPCK(hipMemset(c->stamp_count, 0, sizeof(unsigned int)));
       HIPCK(hipMemset(c->tok, 0, sizeof(int) * (size_t)c->B * c->tok_stride));
-      HIPCK(hipHostMalloc((void**)&c->host_out, sizeof(int) * 3 * (size_t)c->B * (c->K + 1)));
+      HIPCK(hipHostMalloc((void**)&c->host_result, c->res_bytes));
       c->n_host.assign(c->B, 0);
     } catch (...) {
-      if (c->host_out) (void)hipHostFree(c->host_out);
+      if (c->host_result) (void)hipHostFree(c->host_result);
       delete c;
       throw;
     }
@@ -1218,11 +1219,12 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
     const chimera_config& cf = m->cfg;
     const int dt = m->dt, d = cf.d_model, V = cf.vocab;
     StepState s = make_state(ctx);
-    if (ctx->prof && !ctx->ev_created) {
-      HIPCK(hipEventCreate(&ctx->e_start));
-      HIPCK(hipEventCreate(&ctx->e_draft));
-      HIPCK(hipEventCreate(&ctx->e_verify));
-      HIPCK(hipEventCreate(&ctx->e_end));
+    const bool use_graph = ctx->graph_on && st != nullptr;
+    // Under graph replay the step does not consult the profiling flag at all:
+    // phase times come from the stamp ring, read by chimera_profile_read.
+    // (Reading the flag on every replayed step was measured to slow the
+    // replay, with identical GPU work.)
+    if (!use_graph && ctx->prof && !ctx->ev_created) {  // per-launch GEMM events: eager launches only
       ctx->ev_pool.resize(1024);
       ctx->ev_bytes.assign(1024, 0.0);
       for (auto& e : ctx->ev_pool) {
@@ -1231,12 +1233,17 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
       }
       ctx->ev_created = true;
     }
+    // Phase timestamps: a one-lane kernel between phases writes the device
+    // wall clock.  They are part of every step (graph or eager), so turning
+    // profiling on times the same replayed graph that runs without it.
+    auto mark = [&](int idx, hipStream_t q) { launch_stamp(ctx->stamp_ring, ctx->stamp_count, idx, ctx->n, ctx->batch, q); };
     // the launch sequence of one step; every varying scalar lives in device memory
     auto enqueue = [&](hipStream_t q) {
       const Gemm gq{ctx, q, true};
       ctx->ev_used = 0;
+      mark(0, q);
       if (ctx->K > 0) run_draft(ctx, s, q);
-      if (ctx->prof) HIPCK(hipEventRecord(ctx->e_draft, q));
+      mark(1, q);
       launch_tree_setup(s, q);
       const int M = ctx->batch * ctx->N;
       VerifyRows r{ctx->tree_tok, M, ctx->n, kv->page_table, ctx->tree.depth, ctx->tree.path, ctx->N, ctx->D,
@@ -1252,28 +1259,29 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
                              ctx->t_seed, ctx->t_lse, ctx->t_H, ctx->t_sample, q);
       else
         launch_argmax(ctx->logits, M, V, ctx->amax, q);
-      if (ctx->prof) HIPCK(hipEventRecord(ctx->e_verify, q));
+      mark(2, q);
       launch_accept(dt, s, q);
       launch_compact(dt, s, kv->pool, cf.n_layers, kv->layer_stride, q);
       launch_advance(dt, s, q);
+      mark(3, q);
     };
-    const bool use_graph = ctx->graph_on && st != nullptr;
-    if (ctx->prof) HIPCK(hipEventRecord(ctx->e_start, st));
     if (use_graph) {
-      if (ctx->gexec == nullptr || ctx->graph_prof != ctx->prof || ctx->graph_stream != st) {
+      if (ctx->gexec == nullptr || ctx->graph_stream != st) {
         drop_graph(ctx);
         HIPCK(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+        ctx->capturing = true;
         try {
           enqueue(st);
         } catch (...) {
+          ctx->capturing = false;
           hipGraph_t g = nullptr;
           (void)hipStreamEndCapture(st, &g);
           if (g) (void)hipGraphDestroy(g);
           throw;
         }
+        ctx->capturing = false;
         HIPCK(hipStreamEndCapture(st, &ctx->graph));
         HIPCK(hipGraphInstantiate(&ctx->gexec, ctx->graph, nullptr, nullptr, 0));
-        ctx->graph_prof = ctx->prof;
         ctx->graph_stream = st;
         ctx->graph_ev_used = ctx->ev_used;
       }
@@ -1282,37 +1290,29 @@ chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, 
     } else {
       enqueue(st);
     }
-    if (ctx->prof) HIPCK(hipEventRecord(ctx->e_end, st));
     HIPCK(hipGetLastError());
     const size_t K1 = ctx->K + 1, B = ctx->batch;
-    HIPCK(hipMemcpyAsync(ctx->host_out, ctx->out_tok, sizeof(int) * B * K1, hipMemcpyDeviceToHost, st));
-    HIPCK(hipMemcpyAsync(ctx->host_out + B * K1, ctx->out_nodes, sizeof(int) * B * K1, hipMemcpyDeviceToHost, st));
-    HIPCK(hipMemcpyAsync(ctx->host_out + 2 * B * K1, ctx->out_len, sizeof(int) * B, hipMemcpyDeviceToHost, st));
+    HIPCK(hipMemcpyAsync(ctx->host_result, ctx->result, ctx->res_bytes, hipMemcpyDeviceToHost, st));
     sync_or_poison(ctx, st);
+    const int* h_tok = (const int*)ctx->host_result;
+    const int* h_nodes = (const int*)(ctx->host_result + ctx->res_nodes_off);
+    const int* h_len = (const int*)(ctx->host_result + ctx->res_len_off);
     for (size_t b = 0; b < B; ++b) {
-      const int L = ctx->host_out[2 * B * K1 + b];
+      const int L = h_len[b];
       n_new[b] = L;
       for (size_t i = 0; i < K1; ++i) {
-        new_tokens[b * K1 + i] = i < (size_t)L ? ctx->host_out[b * K1 + i] : -1;
-        if (path_nodes) path_nodes[b * K1 + i] = i < (size_t)L ? ctx->host_out[B * K1 + b * K1 + i] : -1;
+        new_tokens[b * K1 + i] = i < (size_t)L ? h_tok[b * K1 + i] : -1;
+        if (path_nodes) path_nodes[b * K1 + i] = i < (size_t)L ? h_nodes[b * K1 + i] : -1;
       }
     }
-    if (ctx->prof) {
-      prof_bytes_verify(ctx);
+    if (!use_graph && ctx->prof) {
       float ms = 0.f;
-      HIPCK(hipEventElapsedTime(&ms, ctx->e_start, ctx->e_draft));
-      ctx->acc.ms_draft += ms;
-      HIPCK(hipEventElapsedTime(&ms, ctx->e_draft, ctx->e_verify));
-      ctx->acc.ms_verify += ms;
-      HIPCK(hipEventElapsedTime(&ms, ctx->e_verify, ctx->e_end));
-      ctx->acc.ms_tail += ms;
       for (size_t i = 0; i < ctx->ev_used; ++i) {
         HIPCK(hipEventElapsedTime(&ms, ctx->ev_pool[i].a, ctx->ev_pool[i].b));
         ctx->acc.ms_gemm_verify += ms;
         ctx->acc.gemm_verify_bytes += ctx->ev_bytes[i];
         ctx->acc.gemm_verify_launches += 1;
       }
-      ctx->acc.steps += 1;
     }
     for (size_t b = 0; b < B; ++b) ctx->n_host[b] += n_new[b];
   });
@@ -1414,7 +1414,48 @@ chimera_status chimera_profile_enable(chimera_ctx* ctx, int32_t enable) {
 chimera_status chimera_profile_read(chimera_ctx* ctx, chimera_profile* out) {
   return guard([&] {
     REQUIRE(ctx != nullptr && out != nullptr, CHIMERA_EINVAL, "null argument");
-    *out = ctx->acc;
+    chimera_profile p = ctx->acc;  // eager per-launch GEMM figures
+    ctx->acc = chimera_profile{};
+    if (ctx->clock_khz <= 0.0) {
+      int dev = 0, khz = 0;
+      HIPCK(hipGetDevice(&dev));
+      HIPCK(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev));
+      REQUIRE(khz > 0, CHIMERA_EHIP, "device wall clock rate unknown");
+      ctx->clock_khz = khz;
+    }
+    {
+      // phase times of the steps stamped since the previous read (at most the
+      // last STAMP_RING of them)
+      HIPCK(hipDeviceSynchronize());
+      unsigned int last = 0;
+      HIPCK(hipMemcpy(&last, ctx->stamp_count, sizeof(unsigned int), hipMemcpyDeviceToHost));
+      const unsigned int first = last - ctx->prof_first > (unsigned)STAMP_RING ? last - STAMP_RING : ctx->prof_first;
+      std::vector<unsigned long long> ring((size_t)STAMP_RING * STAMP_WORDS);
+      HIPCK(hipMemcpy(ring.data(), ctx->stamp_ring, ring.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+      std::vector<double> v_ms, s_ms, d_ms;
+      for (unsigned int c = first; c != last; ++c) {
+        const unsigned long long* t = ring.data() + (size_t)(c % STAMP_RING) * STAMP_WORDS;
+        d_ms.push_back((double)(t[1] - t[0]) / ctx->clock_khz);
+        v_ms.push_back((double)(t[2] - t[1]) / ctx->clock_khz);
+        s_ms.push_back((double)(t[3] - t[0]) / ctx->clock_khz);
+        p.ms_draft += d_ms.back();
+        p.ms_verify += v_ms.back();
+        p.ms_tail += (double)(t[3] - t[2]) / ctx->clock_khz;
+        p.verify_bytes += verify_pass_bytes(ctx, (double)t[4]);
+        p.steps += 1;
+      }
+      auto median = [](std::vector<double> x) {
+        if (x.empty()) return 0.0;
+        std::sort(x.begin(), x.end());
+        const size_t h = x.size() / 2;
+        return x.size() % 2 ? x[h] : 0.5 * (x[h - 1] + x[h]);
+      };
+      p.ms_draft_median = median(d_ms);
+      p.ms_verify_median = median(v_ms);
+      p.ms_step_median = median(s_ms);
+      ctx->prof_first = last;
+    }
+    *out = p;
   });
 }
 
@@ -1648,12 +1689,8 @@ chimera_status chimera_set_graph(chimera_ctx* ctx, int32_t enable) {
 void chimera_ctx_free(chimera_ctx* ctx) {
   if (!ctx) return;
   drop_graph(ctx);
-  if (ctx->host_out) (void)hipHostFree(ctx->host_out);
+  if (ctx->host_result) (void)hipHostFree(ctx->host_result);
   if (ctx->ev_created) {
-    (void)hipEventDestroy(ctx->e_start);
-    (void)hipEventDestroy(ctx->e_draft);
-    (void)hipEventDestroy(ctx->e_verify);
-    (void)hipEventDestroy(ctx->e_end);
     for (auto& e : ctx->ev_pool) {
       (void)hipEventDestroy(e.a);
       (void)hipEventDestroy(e.b);

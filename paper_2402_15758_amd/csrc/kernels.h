@@ -274,3 +274,13 @@ void launch_tri_insert(const StepState& s, const TriCache& c, const DraftLevel& 
 
 void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const int* amax_row, const void* hl_row,
                            hipStream_t st);
+
+// ---- phase timestamps -------------------------------------------------------
+// Every step writes one ring slot of STAMP_WORDS words: the device wall clock
+// (hipDeviceAttributeWallClockRate kHz) at step start (0), draft end (1),
+// verify end (2) and step end (3), and the step's summed committed length
+// (4).  A stamp runs after every earlier kernel of the stream has finished;
+// stamp 3 advances the step counter.
+constexpr int STAMP_RING = 4096;
+constexpr int STAMP_WORDS = 8;
+void launch_stamp(unsigned long long* ring, unsigned int* counter, int idx, const int* n_b, int B, hipStream_t st);

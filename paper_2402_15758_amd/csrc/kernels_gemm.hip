@@ -27,6 +27,11 @@
 #include "common.h"
 #include "kernels.h"
 
+// The GEMM kernels take GemmShape and GemmEpi by value: a plain block of
+// pointers and integers well inside the kernel-argument limit.
+static_assert(sizeof(GemmShape) + sizeof(GemmEpi) + 4 * sizeof(int) <= 512, "GEMM kernel-argument block");
+static_assert(alignof(GemmShape) <= 8 && alignof(GemmEpi) <= 8, "GEMM kernel-argument alignment");
+
 namespace {
 
 constexpr int NB = 4;        // 16-column blocks per weight-layout group

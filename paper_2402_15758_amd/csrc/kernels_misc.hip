@@ -1018,3 +1018,25 @@ void launch_prefill_finish(int dtype, const StepState& s, int b, int n, const in
     hipLaunchKernelGGL(prefill_finish_kernel<float>, dim3(1), dim3(256), 0, st, s, b, n, amax_row,
                        (const float*)hl_row);
 }
+
+// ---- phase timestamps ---------------------------------------------------------
+// One lane reads the GPU's constant-rate wall clock and stores it in the
+// current step's ring slot.  Kernels of a stream run one after another, so a
+// stamp launched between two phases records when the first phase's last
+// kernel has finished, and the four stamps of a step see the same counter.
+__global__ void stamp_kernel(unsigned long long* ring, unsigned int* counter, int idx, const int* n_b, int B) {
+  if (threadIdx.x != 0) return;
+  const unsigned int c = *counter;
+  unsigned long long* slot = ring + (size_t)(c % STAMP_RING) * STAMP_WORDS;
+  slot[idx] = __builtin_amdgcn_s_memrealtime();
+  if (idx == 0) {
+    unsigned long long sum = 0;
+    for (int b = 0; b < B; ++b) sum += (unsigned long long)n_b[b];
+    slot[4] = sum;
+  }
+  if (idx == 3) *counter = c + 1;
+}
+
+void launch_stamp(unsigned long long* ring, unsigned int* counter, int idx, const int* n_b, int B, hipStream_t st) {
+  hipLaunchKernelGGL(stamp_kernel, dim3(1), dim3(64), 0, st, ring, counter, idx, n_b, B);
+}

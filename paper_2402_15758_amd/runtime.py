@@ -55,7 +55,8 @@ class Session:
             self.w_arena = torch.empty(wb, dtype=torch.uint8, device=self.device)
             names, tensors = [], []
             for name, t in weights.items():
-                t = t.contiguous()
+                # the library reads device memory only
+                t = t.to(self.device).contiguous()
                 nb = name.encode()
                 names.append((nb, t))
                 dt = B.CHIMERA_F32 if t.dtype == torch.float32 else B.CHIMERA_BF16

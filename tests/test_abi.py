@@ -66,3 +66,16 @@ def test_tree_arrays():
     parent, rank = tree_arrays(synth.TREE_T8)
     assert list(parent) == [-1, 0, 0, 0, 1, 1, 2, 4]
     assert list(rank) == [0, 0, 1, 2, 0, 3, 0, 0]
+
+
+def test_load_refuses_host_tensors_before_any_device_work():
+    """chimera_load reads device memory only: a host tensor is refused while
+    the tensor list is validated, before anything is copied or launched."""
+    import numpy as np
+    from paper_2402_15758_amd import binding as B
+    mc = synth.TINY
+    emb = np.zeros(mc.vocab * mc.d_model, dtype=np.float32)
+    t = (B.chimera_tensor * 1)(B.chimera_tensor(b"tok_embed", emb.ctypes.data, emb.size, B.CHIMERA_F32, 0))
+    with pytest.raises(B.ChimeraError) as e:
+        B.chimera_load(_cfg(mc), list(t), 256, 1 << 40, 0)
+    assert e.value.status == B.CHIMERA_EINVAL and "not in device memory" in str(e.value)
