@@ -12,7 +12,11 @@ replaced by synthetic prompts and a seeded acceptance bias).  W untimed
 steps run first, then exactly K steps are timed (HIP graph replay, the
 launch mode of the library); the line printed is
 
-  value = accepted (committed) tokens / timed seconds.
+  value = accepted (committed) tokens / timed seconds,
+
+the K steps enqueued back to back (chimera_steps: one host synchronisation
+per up to 64 steps; the same steps one chimera_step call each are reported
+beside it).
 
 Also reported:
   verify_pass  the verify pass (tree pass + LM head + argmax) timed by device
@@ -166,14 +170,30 @@ def counter_traffic():
 
 
 def run_steps(spec, n, out):
-    """n steps; appends each sequence's committed tokens to out; returns the
-    accepted count."""
+    """n steps, one chimera_step call each; appends each sequence's committed
+    tokens to out; returns the accepted count."""
     acc = 0
     for _ in range(n):
         toks, nn, _ = spec.step()
         acc += int(nn.sum())
         for b in range(len(out)):
             out[b] += [int(x) for x in toks[b, : nn[b]]]
+    return acc
+
+
+def run_pipelined(spec, n, out, chunk=64):
+    """n steps enqueued back to back (chimera_steps, up to `chunk` per call);
+    appends each sequence's committed tokens to out; returns the accepted
+    count."""
+    acc, done = 0, 0
+    while done < n:
+        c = min(chunk, n - done)
+        toks, nn, _ = spec.steps(c)
+        acc += int(nn.sum())
+        for i in range(c):
+            for b in range(len(out)):
+                out[b] += [int(x) for x in toks[i, b, : nn[i, b]]]
+        done += c
     return acc
 
 
@@ -193,7 +213,7 @@ def main():
     prompts = wl.prompts()
     B = len(prompts)
     K_levels = max(len(r) for r in synth.TREES[wl.tree])
-    total_steps = a.warmup + 2 * a.steps  # warmup, timed pass, eager-profiled pass
+    total_steps = a.warmup + 3 * a.steps  # warmup, timed pass, one-call-per-step pass, eager-profiled pass
     horizon = max(total_steps * (K_levels + 1), wl.gen_tokens + K_levels + 1)
     max_len = max(len(p) for p in prompts) + horizon + 128
     max_len = (max_len + 63) // 64 * 64
@@ -214,10 +234,7 @@ def main():
     streams = [[int(t)] for t in ar.prefill(prompts)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    while min(len(s) for s in streams) < n_ref:
-        toks, n, _ = ar.step()
-        for b in range(B):
-            streams[b] += [int(x) for x in toks[b, : n[b]]]
+    run_pipelined(ar, n_ref - 1, streams)  # one token per greedy step
     torch.cuda.synchronize()
     ar_rate = B * (n_ref - 1) / (time.perf_counter() - t0)
     stride = max_len + 8
@@ -227,16 +244,23 @@ def main():
     log(f"[bench] spec: prefill, {a.warmup} warmup steps, {a.steps} timed steps")
     out = [[int(t)] for t in spec.prefill(prompts)]
     run_steps(spec, a.warmup, out)
-    # timed pass: exactly K steps, graph replay.  Every step carries one-lane
-    # wall-clock stamp kernels at its phase boundaries (draft | verify | tail);
-    # the library reports the per-step medians of exactly these steps.
+    # timed pass: exactly K steps, graph replay, enqueued back to back
+    # (chimera_steps).  Every step carries one-lane wall-clock stamp kernels
+    # at its phase boundaries (draft | verify | tail); the library reports the
+    # per-step medians of exactly these steps.
     spec.profile_read()  # opens the stamp window
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    accepted = run_steps(spec, a.steps, out)
+    accepted = run_pipelined(spec, a.steps, out)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     prof_g = spec.profile_read()
+    # the same K steps with one host round trip per step (chimera_step)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    accepted_1 = run_steps(spec, a.steps, out)
+    torch.cuda.synchronize()
+    dt_1 = time.perf_counter() - t0
     # eager-profiled pass: kernels launched one by one, each verify GEMM
     # launch recording HIP events at its own dispatch start and end
     spec.set_graph(False)
@@ -257,8 +281,12 @@ def main():
         t0 = time.perf_counter()
         steps = 0
         while min(len(x) for x in o) < wl.gen_tokens:
-            run_steps(spec, 1, o)
-            steps += 1
+            # every step commits 1 .. K+1 tokens: enqueue as many steps as the
+            # remainder surely needs
+            need = wl.gen_tokens - min(len(x) for x in o)
+            c = max(1, -(-need // (K_levels + 1)))
+            run_pipelined(spec, c, o)
+            steps += c
         torch.cuda.synchronize()
         t_gen = time.perf_counter() - t0
         committed = sum(len(x) - 1 for x in o)
@@ -269,7 +297,7 @@ def main():
                   "tokens_per_s_median": round(gen_sorted[1][0], 2),
                   "tokens_per_s": [round(g[0], 2) for g in gen],
                   "steps": [g[1] for g in gen], "committed": [g[2] for g in gen],
-                  "timing": "first chimera_step to the last synchronisation, prefill excluded"}
+                  "timing": "pipelined steps (chimera_steps), first launch to the last synchronisation, prefill excluded"}
     log(f"[bench] generation of {wl.gen_tokens} tokens x3: {generation['tokens_per_s']} tok/s")
 
     tri = None
@@ -441,6 +469,8 @@ def main():
             "timing": "device wall-clock stamps around the verify pass inside the replayed step graph, median over the timed steps",
         },
         "step_ms_stamped_median": round(prof_g.ms_step_median, 4),
+        "one_call_per_step": {"tokens_per_s": round(accepted_1 / dt_1, 2),
+                              "ms_per_step": round(dt_1 / a.steps * 1e3, 4)},
         "copy_bw_gbs": round(copy_gbs, 1),
         "draft_ms": round(prof_g.ms_draft_median, 4),
         "tail_ms": round(prof_g.ms_tail / max(prof_g.steps, 1), 4),

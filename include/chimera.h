@@ -135,6 +135,20 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
 chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, int32_t* new_tokens,
                             int32_t* n_new, int32_t* path_nodes, void* stream);
 
+/* Pipelined decoding: n_steps consecutive chimera_step iterations enqueued
+ * back to back on `stream`, each step's results copied asynchronously to
+ * its own host slot, with one synchronisation at the end.  Every input a
+ * step needs lives in device memory, so no step waits for the host.
+ * Outputs (host): new_tokens [n_steps][batch][K+1], n_new [n_steps][batch],
+ * path_nodes [n_steps][batch][K+1] (nullable), each step as chimera_step
+ * reports it.  n_steps in [1, CHIMERA_MAX_PIPELINED_STEPS]; the capacity
+ * check assumes every step accepts K+1 tokens (CHIMERA_ECAPACITY before
+ * any launch otherwise).  Results are identical to n_steps chimera_step
+ * calls.  Synchronises `stream`. */
+#define CHIMERA_MAX_PIPELINED_STEPS 64
+chimera_status chimera_steps(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, int32_t n_steps, int32_t* new_tokens,
+                             int32_t* n_new, int32_t* path_nodes, void* stream);
+
 /* ---- benchmarking and parity hooks --------------------------------------
  * Forced acceptance (synthetic workloads): at draft level k of a step with
  * committed length n the predicted position is j = n+1+k; if ok[b*stride+j]

@@ -13,6 +13,7 @@ CHIMERA_F32, CHIMERA_BF16 = 0, 1
 CHIMERA_DECODE_GREEDY, CHIMERA_DECODE_TYPICAL = 0, 1
 CHIMERA_DRAFT_CHAIN, CHIMERA_DRAFT_BRANCH = 0, 1
 DBG_VERIFY_LOGITS, DBG_DRAFT_LOGITS, DBG_TREE_TOKENS, DBG_DRAFT_LISTS, DBG_SEQ_LEN, DBG_TOKENS = range(6)
+CHIMERA_MAX_PIPELINED_STEPS = 64
 CHIMERA_OK, CHIMERA_EINVAL, CHIMERA_ENOMEM, CHIMERA_ECAPACITY, CHIMERA_EHIP, CHIMERA_ESTATE = 0, -1, -2, -3, -4, -5
 STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "ECAPACITY", -4: "EHIP", -5: "ESTATE"}
 
@@ -59,6 +60,7 @@ _PROTOS = {
     "chimera_ctx_create": [P, P, PI32, PI32, I32, P, I64, ctypes.POINTER(P)],
     "chimera_prefill": [P, P, P, PI32, PI32, I32, PI32, P],
     "chimera_step": [P, P, P, PI32, PI32, PI32, P],
+    "chimera_steps": [P, P, P, I32, PI32, PI32, PI32, P],
     "chimera_set_forcing": [P, P, P, I32],
     "chimera_set_tree_tokens": [P, PI32, I32],
     "chimera_debug_copy": [P, I32, P, I64],
@@ -158,6 +160,11 @@ def chimera_prefill(model: int, kv: int, ctx: int, tokens, lens, first_tokens, s
 
 def chimera_step(model: int, kv: int, ctx: int, new_tokens, n_new, path_nodes, stream: int):
     _check(lib().chimera_step(model, kv, ctx, _i32p(new_tokens), _i32p(n_new), _i32p(path_nodes), stream))
+
+
+def chimera_steps(model: int, kv: int, ctx: int, n_steps: int, new_tokens, n_new, path_nodes, stream: int):
+    _check(lib().chimera_steps(model, kv, ctx, n_steps, _i32p(new_tokens), _i32p(n_new), _i32p(path_nodes),
+                               stream))
 
 
 def chimera_set_forcing(ctx: int, ref_ptr, ok_ptr, stride: int):

@@ -236,6 +236,7 @@ struct chimera_ctx {
   // context was sized for).
   char* result = nullptr;
   char* host_result = nullptr;  // pinned mirror
+  char* host_pipe = nullptr;    // pinned [CHIMERA_MAX_PIPELINED_STEPS] result blocks (chimera_steps)
   size_t res_bytes = 0, res_nodes_off = 0, res_len_off = 0;
   // profiling
   bool prof = false;
@@ -1103,9 +1104,11 @@ chimera_status chimera_ctx_create(chimera_model* m, chimera_kv* kv, const int32_
       HIPCK(hipMemset(c->stamp_count, 0, sizeof(unsigned int)));
       HIPCK(hipMemset(c->tok, 0, sizeof(int) * (size_t)c->B * c->tok_stride));
       HIPCK(hipHostMalloc((void**)&c->host_result, c->res_bytes));
+      HIPCK(hipHostMalloc((void**)&c->host_pipe, c->res_bytes * CHIMERA_MAX_PIPELINED_STEPS));
       c->n_host.assign(c->B, 0);
     } catch (...) {
       if (c->host_result) (void)hipHostFree(c->host_result);
+      if (c->host_pipe) (void)hipHostFree(c->host_pipe);
       delete c;
       throw;
     }
@@ -1205,116 +1208,176 @@ chimera_status chimera_prefill(chimera_model* m, chimera_kv* kv, chimera_ctx* ct
   });
 }
 
+}  // extern "C"
+
+namespace {
+
+// Enqueue one draft -> verify -> accept -> compact step on st: replay of the
+// captured graph (captured on first use) or eager launches.
+void enqueue_step(chimera_ctx* ctx, hipStream_t st) {
+  chimera_model* m = ctx->m;
+  chimera_kv* kv = ctx->kv;
+  const chimera_config& cf = m->cfg;
+  const int dt = m->dt, d = cf.d_model, V = cf.vocab;
+  StepState s = make_state(ctx);
+  const bool use_graph = ctx->graph_on && st != nullptr;
+  // Under graph replay the step does not consult the profiling flag at all:
+  // phase times come from the stamp ring, read by chimera_profile_read.
+  // (Reading the flag on every replayed step was measured to slow the
+  // replay, with identical GPU work.)
+  if (!use_graph && ctx->prof && !ctx->ev_created) {  // per-launch GEMM events: eager launches only
+    ctx->ev_pool.resize(1024);
+    ctx->ev_bytes.assign(1024, 0.0);
+    for (auto& e : ctx->ev_pool) {
+      HIPCK(hipEventCreate(&e.a));
+      HIPCK(hipEventCreate(&e.b));
+    }
+    ctx->ev_created = true;
+  }
+  // Phase timestamps: a one-lane kernel between phases writes the device
+  // wall clock.  They are part of every step (graph or eager), so turning
+  // profiling on times the same replayed graph that runs without it.
+  auto mark = [&](int idx, hipStream_t q) { launch_stamp(ctx->stamp_ring, ctx->stamp_count, idx, ctx->n, ctx->batch, q); };
+  // the launch sequence of one step; every varying scalar lives in device memory
+  auto enqueue = [&](hipStream_t q) {
+    const Gemm gq{ctx, q, true};
+    ctx->ev_used = 0;
+    mark(0, q);
+    if (ctx->K > 0) run_draft(ctx, s, q);
+    mark(1, q);
+    launch_tree_setup(s, q);
+    const int M = ctx->batch * ctx->N;
+    VerifyRows r{ctx->tree_tok, M, ctx->n, kv->page_table, ctx->tree.depth, ctx->tree.path, ctx->N, ctx->D,
+                 ctx->batch};
+    verify_layers(ctx, r, q, true);
+    GemmEpi el;
+    el.kind = EPI_F32;
+    el.out_f = ctx->logits;
+    el.ldo = V;
+    gq.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
+    if (ctx->typical)
+      launch_typical_stats(ctx->logits, M, V, ctx->N, 0, ctx->n, ctx->tree.depth, -1, 1.f / ctx->temperature,
+                           ctx->t_seed, ctx->t_lse, ctx->t_H, ctx->t_sample, q);
+    else
+      launch_argmax(ctx->logits, M, V, ctx->amax, q);
+    mark(2, q);
+    launch_accept(dt, s, q);
+    launch_compact(dt, s, kv->pool, cf.n_layers, kv->layer_stride, q);
+    launch_advance(dt, s, q);
+    mark(3, q);
+  };
+  if (use_graph) {
+    if (ctx->gexec == nullptr || ctx->graph_stream != st) {
+      drop_graph(ctx);
+      HIPCK(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+      ctx->capturing = true;
+      try {
+        enqueue(st);
+      } catch (...) {
+        ctx->capturing = false;
+        hipGraph_t g = nullptr;
+        (void)hipStreamEndCapture(st, &g);
+        if (g) (void)hipGraphDestroy(g);
+        throw;
+      }
+      ctx->capturing = false;
+      HIPCK(hipStreamEndCapture(st, &ctx->graph));
+      HIPCK(hipGraphInstantiate(&ctx->gexec, ctx->graph, nullptr, nullptr, 0));
+      ctx->graph_stream = st;
+      ctx->graph_ev_used = ctx->ev_used;
+    }
+    ctx->ev_used = ctx->graph_ev_used;
+    HIPCK(hipGraphLaunch(ctx->gexec, st));
+  } else {
+    enqueue(st);
+  }
+  HIPCK(hipGetLastError());
+}
+
+// One step's outputs from a host copy of the result block.
+void parse_result(const chimera_ctx* ctx, const char* block, int32_t* new_tokens, int32_t* n_new,
+                  int32_t* path_nodes) {
+  const size_t K1 = ctx->K + 1, B = ctx->batch;
+  const int* h_tok = (const int*)block;
+  const int* h_nodes = (const int*)(block + ctx->res_nodes_off);
+  const int* h_len = (const int*)(block + ctx->res_len_off);
+  for (size_t b = 0; b < B; ++b) {
+    const int L = h_len[b];
+    n_new[b] = L;
+    for (size_t i = 0; i < K1; ++i) {
+      new_tokens[b * K1 + i] = i < (size_t)L ? h_tok[b * K1 + i] : -1;
+      if (path_nodes) path_nodes[b * K1 + i] = i < (size_t)L ? h_nodes[b * K1 + i] : -1;
+    }
+  }
+}
+
+// Per-launch GEMM events of an eagerly launched, profiled step (after its sync).
+void collect_gemm_events(chimera_ctx* ctx, hipStream_t st) {
+  const bool use_graph = ctx->graph_on && st != nullptr;
+  if (use_graph || !ctx->prof) return;
+  float ms = 0.f;
+  for (size_t i = 0; i < ctx->ev_used; ++i) {
+    HIPCK(hipEventElapsedTime(&ms, ctx->ev_pool[i].a, ctx->ev_pool[i].b));
+    ctx->acc.ms_gemm_verify += ms;
+    ctx->acc.gemm_verify_bytes += ctx->ev_bytes[i];
+    ctx->acc.gemm_verify_launches += 1;
+  }
+}
+
+void check_step_call(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, int n_steps) {
+  check_ctx(ctx);
+  REQUIRE(m == ctx->m && kv == ctx->kv, CHIMERA_EINVAL, "ctx belongs to another model/kv");
+  REQUIRE(ctx->batch >= 1, CHIMERA_ESTATE, "chimera_step before chimera_prefill");
+  for (int b = 0; b < ctx->batch; ++b)
+    REQUIRE(ctx->n_host[b] + (int64_t)(n_steps - 1) * (ctx->K + 1) + ctx->N + ctx->K + 2 <= kv->max_len,
+            CHIMERA_ECAPACITY, "sequence would outgrow its KV capacity");
+}
+
+}  // namespace
+
+extern "C" {
+
 chimera_status chimera_step(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, int32_t* new_tokens, int32_t* n_new,
                             int32_t* path_nodes, void* stream) {
   return guard([&] {
-    check_ctx(ctx);
-    REQUIRE(m == ctx->m && kv == ctx->kv, CHIMERA_EINVAL, "ctx belongs to another model/kv");
+    check_step_call(m, kv, ctx, 1);
     REQUIRE(new_tokens != nullptr && n_new != nullptr, CHIMERA_EINVAL, "null output");
-    REQUIRE(ctx->batch >= 1, CHIMERA_ESTATE, "chimera_step before chimera_prefill");
-    for (int b = 0; b < ctx->batch; ++b)
-      REQUIRE(ctx->n_host[b] + ctx->N + ctx->K + 2 <= kv->max_len, CHIMERA_ECAPACITY,
-              "sequence would outgrow its KV capacity");
     hipStream_t st = (hipStream_t)stream;
-    const chimera_config& cf = m->cfg;
-    const int dt = m->dt, d = cf.d_model, V = cf.vocab;
-    StepState s = make_state(ctx);
-    const bool use_graph = ctx->graph_on && st != nullptr;
-    // Under graph replay the step does not consult the profiling flag at all:
-    // phase times come from the stamp ring, read by chimera_profile_read.
-    // (Reading the flag on every replayed step was measured to slow the
-    // replay, with identical GPU work.)
-    if (!use_graph && ctx->prof && !ctx->ev_created) {  // per-launch GEMM events: eager launches only
-      ctx->ev_pool.resize(1024);
-      ctx->ev_bytes.assign(1024, 0.0);
-      for (auto& e : ctx->ev_pool) {
-        HIPCK(hipEventCreate(&e.a));
-        HIPCK(hipEventCreate(&e.b));
-      }
-      ctx->ev_created = true;
-    }
-    // Phase timestamps: a one-lane kernel between phases writes the device
-    // wall clock.  They are part of every step (graph or eager), so turning
-    // profiling on times the same replayed graph that runs without it.
-    auto mark = [&](int idx, hipStream_t q) { launch_stamp(ctx->stamp_ring, ctx->stamp_count, idx, ctx->n, ctx->batch, q); };
-    // the launch sequence of one step; every varying scalar lives in device memory
-    auto enqueue = [&](hipStream_t q) {
-      const Gemm gq{ctx, q, true};
-      ctx->ev_used = 0;
-      mark(0, q);
-      if (ctx->K > 0) run_draft(ctx, s, q);
-      mark(1, q);
-      launch_tree_setup(s, q);
-      const int M = ctx->batch * ctx->N;
-      VerifyRows r{ctx->tree_tok, M, ctx->n, kv->page_table, ctx->tree.depth, ctx->tree.path, ctx->N, ctx->D,
-                   ctx->batch};
-      verify_layers(ctx, r, q, true);
-      GemmEpi el;
-      el.kind = EPI_F32;
-      el.out_f = ctx->logits;
-      el.ldo = V;
-      gq.run(ctx->hl, ctx->mt_v, M, m->lm_head, V, d, el);
-      if (ctx->typical)
-        launch_typical_stats(ctx->logits, M, V, ctx->N, 0, ctx->n, ctx->tree.depth, -1, 1.f / ctx->temperature,
-                             ctx->t_seed, ctx->t_lse, ctx->t_H, ctx->t_sample, q);
-      else
-        launch_argmax(ctx->logits, M, V, ctx->amax, q);
-      mark(2, q);
-      launch_accept(dt, s, q);
-      launch_compact(dt, s, kv->pool, cf.n_layers, kv->layer_stride, q);
-      launch_advance(dt, s, q);
-      mark(3, q);
-    };
-    if (use_graph) {
-      if (ctx->gexec == nullptr || ctx->graph_stream != st) {
-        drop_graph(ctx);
-        HIPCK(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
-        ctx->capturing = true;
-        try {
-          enqueue(st);
-        } catch (...) {
-          ctx->capturing = false;
-          hipGraph_t g = nullptr;
-          (void)hipStreamEndCapture(st, &g);
-          if (g) (void)hipGraphDestroy(g);
-          throw;
-        }
-        ctx->capturing = false;
-        HIPCK(hipStreamEndCapture(st, &ctx->graph));
-        HIPCK(hipGraphInstantiate(&ctx->gexec, ctx->graph, nullptr, nullptr, 0));
-        ctx->graph_stream = st;
-        ctx->graph_ev_used = ctx->ev_used;
-      }
-      ctx->ev_used = ctx->graph_ev_used;
-      HIPCK(hipGraphLaunch(ctx->gexec, st));
-    } else {
-      enqueue(st);
-    }
-    HIPCK(hipGetLastError());
-    const size_t K1 = ctx->K + 1, B = ctx->batch;
+    enqueue_step(ctx, st);
     HIPCK(hipMemcpyAsync(ctx->host_result, ctx->result, ctx->res_bytes, hipMemcpyDeviceToHost, st));
     sync_or_poison(ctx, st);
-    const int* h_tok = (const int*)ctx->host_result;
-    const int* h_nodes = (const int*)(ctx->host_result + ctx->res_nodes_off);
-    const int* h_len = (const int*)(ctx->host_result + ctx->res_len_off);
-    for (size_t b = 0; b < B; ++b) {
-      const int L = h_len[b];
-      n_new[b] = L;
-      for (size_t i = 0; i < K1; ++i) {
-        new_tokens[b * K1 + i] = i < (size_t)L ? h_tok[b * K1 + i] : -1;
-        if (path_nodes) path_nodes[b * K1 + i] = i < (size_t)L ? h_nodes[b * K1 + i] : -1;
+    parse_result(ctx, ctx->host_result, new_tokens, n_new, path_nodes);
+    collect_gemm_events(ctx, st);
+    for (int b = 0; b < ctx->batch; ++b) ctx->n_host[b] += n_new[b];
+  });
+}
+
+chimera_status chimera_steps(chimera_model* m, chimera_kv* kv, chimera_ctx* ctx, int32_t n_steps, int32_t* new_tokens,
+                             int32_t* n_new, int32_t* path_nodes, void* stream) {
+  return guard([&] {
+    REQUIRE(n_steps >= 1 && n_steps <= CHIMERA_MAX_PIPELINED_STEPS, CHIMERA_EINVAL, "n_steps in [1, 64]");
+    check_step_call(m, kv, ctx, n_steps);
+    REQUIRE(new_tokens != nullptr && n_new != nullptr, CHIMERA_EINVAL, "null output");
+    hipStream_t st = (hipStream_t)stream;
+    const size_t B = ctx->batch, K1 = ctx->K + 1;
+    // eager launches with per-launch events reuse one event set per step:
+    // those steps synchronise one at a time
+    const bool each = !(ctx->graph_on && st != nullptr) && ctx->prof;
+    for (int i = 0; i < n_steps; ++i) {
+      enqueue_step(ctx, st);
+      HIPCK(hipMemcpyAsync(ctx->host_pipe + (size_t)i * ctx->res_bytes, ctx->result, ctx->res_bytes,
+                           hipMemcpyDeviceToHost, st));
+      if (each) {
+        sync_or_poison(ctx, st);
+        collect_gemm_events(ctx, st);
       }
     }
-    if (!use_graph && ctx->prof) {
-      float ms = 0.f;
-      for (size_t i = 0; i < ctx->ev_used; ++i) {
-        HIPCK(hipEventElapsedTime(&ms, ctx->ev_pool[i].a, ctx->ev_pool[i].b));
-        ctx->acc.ms_gemm_verify += ms;
-        ctx->acc.gemm_verify_bytes += ctx->ev_bytes[i];
-        ctx->acc.gemm_verify_launches += 1;
-      }
+    sync_or_poison(ctx, st);
+    for (int i = 0; i < n_steps; ++i) {
+      parse_result(ctx, ctx->host_pipe + (size_t)i * ctx->res_bytes, new_tokens + i * B * K1, n_new + i * B,
+                   path_nodes ? path_nodes + i * B * K1 : nullptr);
+      for (size_t b = 0; b < B; ++b) ctx->n_host[b] += n_new[i * B + b];
     }
-    for (size_t b = 0; b < B; ++b) ctx->n_host[b] += n_new[b];
   });
 }
 
@@ -1690,6 +1753,7 @@ void chimera_ctx_free(chimera_ctx* ctx) {
   if (!ctx) return;
   drop_graph(ctx);
   if (ctx->host_result) (void)hipHostFree(ctx->host_result);
+  if (ctx->host_pipe) (void)hipHostFree(ctx->host_pipe);
   if (ctx->ev_created) {
     for (auto& e : ctx->ev_pool) {
       (void)hipEventDestroy(e.a);

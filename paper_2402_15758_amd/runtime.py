@@ -100,6 +100,16 @@ class Session:
         B.chimera_step(self.model, self.kv, self.ctx, toks, n, path, self.stream())
         return toks, n, path
 
+    def steps(self, n: int):
+        """n pipelined steps (chimera_steps, at most CHIMERA_MAX_PIPELINED_STEPS
+        per call): arrays [n][batch][K+1], [n][batch], [n][batch][K+1]."""
+        K1 = self.K + 1
+        toks = np.zeros((n, self.batch, K1), dtype=np.int32)
+        nn = np.zeros((n, self.batch), dtype=np.int32)
+        path = np.zeros((n, self.batch, K1), dtype=np.int32)
+        B.chimera_steps(self.model, self.kv, self.ctx, n, toks, nn, path, self.stream())
+        return toks, nn, path
+
     def generate(self, prompts: List[np.ndarray], n_new: int):
         """Prefill, then step until every sequence has n_new tokens; returns
         (per-sequence token lists truncated to n_new, per-step records)."""

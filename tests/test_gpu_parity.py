@@ -302,6 +302,78 @@ def test_small_bf16_graph_equals_eager(small):
         assert np.array_equal(la.view(np.uint32), lb.view(np.uint32))
 
 
+def test_small_bf16_pipelined_steps_equal_single_steps(small):
+    """chimera_steps (steps enqueued back to back, one synchronisation)
+    returns exactly what one chimera_step call per step returns: batch of 3
+    ragged sequences, forced acceptance, graph replay and eager launches with
+    per-launch events; the committed tokens and the last verify logits
+    match bit for bit."""
+    import torch
+    from paper_2402_15758_amd import binding as B
+    w, _ = small
+    log("small bf16: pipelined steps vs single steps, batch 3, 14 steps")
+    lens = [70, 130, 200]
+    prompts = [synth.make_prompt(n, SMALL.vocab, 600 + n) for n in lens]
+    max_len = 512
+    stride = max_len + 8
+    ar_s = make_session(SMALL, w, (), max_batch=3, max_len=max_len)
+    out_a, _ = ar_s.generate(prompts, 90)
+    ar_s.close()
+    ref = np.full((3, stride), -1, dtype=np.int32)
+    ok = np.stack([synth.force_table(p, 5, b, stride) for b, p in enumerate([0.5, 0.8, 0.95])])
+    for b, n in enumerate(lens):
+        ref[b, n:n + 90] = out_a[b]
+    runs = {}
+    for mode in ("single", "pipelined", "pipelined_eager_profiled"):
+        sp = make_session(SMALL, w, synth.TREE_T32, max_batch=3, max_len=max_len)
+        sp.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+        if mode == "pipelined_eager_profiled":
+            sp.set_graph(False)
+            sp.profile(True)
+        sp.prefill(prompts)
+        if mode == "single":
+            rec = [sp.step() for _ in range(14)]
+            toks = np.stack([r[0] for r in rec])
+            nn = np.stack([r[1] for r in rec])
+            path = np.stack([r[2] for r in rec])
+        else:
+            a = sp.steps(5)
+            b = sp.steps(9)
+            toks, nn, path = (np.concatenate([x, y]) for x, y in zip(a, b))
+        if mode == "pipelined_eager_profiled":
+            pr = sp.profile_read()
+            assert pr.steps == 14 and pr.gemm_verify_launches > 0
+        runs[mode] = (toks, nn, path, sp.debug(B.DBG_TOKENS), sp.debug(B.DBG_VERIFY_LOGITS))
+        sp.close()
+    base = runs["single"]
+    for mode in ("pipelined", "pipelined_eager_profiled"):
+        for x, y in zip(base, runs[mode]):
+            assert np.array_equal(np.ascontiguousarray(x).view(np.uint32), np.ascontiguousarray(y).view(np.uint32)), mode
+    assert base[1].min() >= 1 and base[1].max() > 1
+    # lossless: each sequence's stream is its greedy stream
+    for b in range(3):
+        got = [int(t) for i in range(14) for t in base[0][i, b, : base[1][i, b]]]
+        assert got == out_a[b][1: 1 + len(got)]
+
+
+def test_pipelined_steps_refuse_bad_counts(small):
+    from paper_2402_15758_amd import binding as B
+    w, _ = small
+    sp = make_session(SMALL, w, synth.TREE_T32, max_len=256)
+    sp.prefill([synth.make_prompt(40, SMALL.vocab, 9)])
+    for n in (0, B.CHIMERA_MAX_PIPELINED_STEPS + 1):
+        with pytest.raises(B.ChimeraError) as e:
+            B.chimera_steps(sp.model, sp.kv, sp.ctx, n, np.zeros(8, np.int32), np.zeros(8, np.int32), None,
+                            sp.stream())
+        assert e.value.status == B.CHIMERA_EINVAL
+    with pytest.raises(B.ChimeraError) as e:
+        sp.steps(60)  # 60 steps of up to 5 tokens would outgrow the 256-token capacity
+    assert e.value.status == B.CHIMERA_ECAPACITY
+    toks, nn, _ = sp.step()  # the refused calls changed nothing
+    assert nn[0] >= 1
+    sp.close()
+
+
 # ---------------------------------------------------------------------------
 # Trigram lookup cache (Sec. 4.1.1): exact memoization of the trigram encoder
 # ---------------------------------------------------------------------------
