@@ -60,6 +60,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama7b_p512")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-generation", action="store_true", help="skip the three whole-generation timings")
+    ap.add_argument("--counter-sample", action="store_true",
+                    help="only a short sample for hardware-counter passes: the workload's model and tree, "
+                         "64-token prompts, three steps launched kernel by kernel, then three 1 GiB device "
+                         "copies (the counters' scale reference); prints no benchmark line")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--no-typical", action="store_true", help="skip the typical-decoding (T = 1) measurement")
@@ -225,6 +230,21 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] weights ready in {time.perf_counter() - t0:.1f}s; loading")
     spec = Session(cfg, weights, synth.TREES[wl.tree], max_batch=B, max_len=max_len)
+    if a.counter_sample:
+        # the same verify-pass kernels at the workload's rows (batch x tree
+        # nodes); a short context keeps the number of dispatches small
+        spec.set_graph(False)
+        spec.prefill([p[:64] for p in prompts])
+        for _ in range(3):
+            spec.step()
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] counter sample: {wl.name}, {B} x 64-token prompts, 3 eager steps, 3 x 1 GiB copies")
+        spec.close()
+        return
     ar = Session(cfg, None, (), max_batch=B, max_len=max_len, share_model=spec)
     torch.cuda.synchronize()
 
@@ -275,7 +295,7 @@ def main():
 
     # the whole generation: G tokens per sequence after the prefill, three times
     gen = []
-    for rep in range(3):
+    for rep in range(0 if a.no_generation else 3):
         o = [[int(t)] for t in spec.prefill(prompts)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -293,12 +313,13 @@ def main():
         gen.append((committed / t_gen, steps, committed, t_gen))
         lossless = lossless and all(o[b] == streams[b][: len(o[b])] for b in range(B))
     gen_sorted = sorted(gen)
-    generation = {"tokens": wl.gen_tokens, "reps": 3,
+    generation = None if not gen else {"tokens": wl.gen_tokens, "reps": 3,
                   "tokens_per_s_median": round(gen_sorted[1][0], 2),
                   "tokens_per_s": [round(g[0], 2) for g in gen],
                   "steps": [g[1] for g in gen], "committed": [g[2] for g in gen],
                   "timing": "pipelined steps (chimera_steps), first launch to the last synchronisation, prefill excluded"}
-    log(f"[bench] generation of {wl.gen_tokens} tokens x3: {generation['tokens_per_s']} tok/s")
+    if generation:
+        log(f"[bench] generation of {wl.gen_tokens} tokens x3: {generation['tokens_per_s']} tok/s")
 
     tri = None
     if a.trigram_cache:
