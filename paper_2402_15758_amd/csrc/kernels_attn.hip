@@ -245,21 +245,25 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
         const int4 hfrag = int4{(int)ph[0], (int)ph[1], (int)ph[2], (int)ph[3]};
         const int4 mfrag = int4{(int)pm[0], (int)pm[1], (int)pm[2], (int)pm[3]};
         const int4 lfrag = int4{(int)pl[0], (int)pl[1], (int)pl[2], (int)pl[3]};
-        int4 vf[HD / 16];
+        // V^T fragments two output blocks at a time; within a pair the terms
+        // alternate between the two accumulators
 #pragma unroll
-        for (int db = 0; db < HD / 16; ++db) {
-          const T* vr = &Vt[(16 * db + c16) * VP];
-          const int2 lo = *reinterpret_cast<const int2*>(vr + 32 * kp + 4 * g);
-          const int2 hi = *reinterpret_cast<const int2*>(vr + 32 * kp + 16 + 4 * g);
-          vf[db] = int4{lo.x, lo.y, hi.x, hi.y};
+        for (int d2 = 0; d2 < HD / 16; d2 += 2) {
+          int4 vf[2];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const T* vr = &Vt[(16 * (d2 + j) + c16) * VP];
+            const int2 lo = *reinterpret_cast<const int2*>(vr + 32 * kp + 4 * g);
+            const int2 hi = *reinterpret_cast<const int2*>(vr + 32 * kp + 16 + 4 * g);
+            vf[j] = int4{lo.x, lo.y, hi.x, hi.y};
+          }
+          o[d2] = mfma_kb<T>(vf[0], hfrag, o[d2]);
+          o[d2 + 1] = mfma_kb<T>(vf[1], hfrag, o[d2 + 1]);
+          o[d2] = mfma_kb<T>(vf[0], mfrag, o[d2]);
+          o[d2 + 1] = mfma_kb<T>(vf[1], mfrag, o[d2 + 1]);
+          o[d2] = mfma_kb<T>(vf[0], lfrag, o[d2]);
+          o[d2 + 1] = mfma_kb<T>(vf[1], lfrag, o[d2 + 1]);
         }
-        // term-major: consecutive MFMAs update different accumulators
-#pragma unroll
-        for (int db = 0; db < HD / 16; ++db) o[db] = mfma_kb<T>(vf[db], hfrag, o[db]);
-#pragma unroll
-        for (int db = 0; db < HD / 16; ++db) o[db] = mfma_kb<T>(vf[db], mfrag, o[db]);
-#pragma unroll
-        for (int db = 0; db < HD / 16; ++db) o[db] = mfma_kb<T>(vf[db], lfrag, o[db]);
       }
     } else {
 #pragma unroll

@@ -590,9 +590,20 @@ void gemm_t(const GemmShape& s, const GemmEpi& e, hipStream_t st, hipEvent_t ev_
     gemm_mb<T, 1>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   else if (s.M <= 32)
     gemm_mb<T, 2>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
-  else if (s.M > 64 && cba <= CB_MAX_MB8 && (s.M + 127) / 128 * 8 <= s.x_mtiles)
-    gemm_mb8<T>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
-  else
+  else if (s.M > 64 && cba <= CB_MAX_MB8 && (s.M + 127) / 128 * 8 <= s.x_mtiles) {
+    // A 128-row workgroup holds one CU on its own.  When runs of up to
+    // CB_MAX_MB8 blocks let the whole launch (row blocks x runs x splits) fit
+    // one workgroup per CU, deal the columns that way: a single round beats
+    // two rounds of shorter runs, each re-reading the activation tiles.
+    const int gx = (s.M + 127) / 128;
+    const int nwg1 = std::max((nbc + CB_MAX_MB8 - 1) / CB_MAX_MB8, GEMM_WGS / (gx * s.splits));
+    if (nwg1 < nwg && gx * nwg1 * s.splits <= GEMM_WGS) {
+      const int cba1 = (nbc + nwg1 - 1) / nwg1;
+      gemm_mb8<T>(s, e, kind, nwg1, cba1, nbc - nwg1 * (cba1 - 1), st, ev_start, eb);
+    } else {
+      gemm_mb8<T>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
+    }
+  } else
     gemm_mb<T, 4>(s, e, kind, nwg, cba, nbig, st, ev_start, eb);
   if (finish) {
     const int64_t total = (int64_t)s.M * nbc * 16;
