@@ -69,6 +69,8 @@ def parse():
                     help="also run a 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--no-typical", action="store_true", help="skip the typical-decoding (T = 1) measurement")
     ap.add_argument("--no-branch", action="store_true", help="skip the branch-conditioned drafting measurement")
+    ap.add_argument("--torch-gemm-reference", action="store_true",
+                    help="also time torch's bf16 linear (hipBLASLt) on the verify GEMM shapes, as a library reference")
     ap.add_argument("--trigram-cache", type=int, default=65536,
                     help="entries of the trigram lookup cache measured after the headline passes (0: skip)")
     return ap.parse_args()
@@ -152,6 +154,35 @@ def copy_bandwidth(torch, dev, nbytes=1 << 30, reps=5):
         best = ms if best is None else min(best, ms)
     del src, dst
     return 2.0 * nbytes / (best * 1e-3) / 1e9
+
+
+def torch_gemm_reference(torch, dev, cfg, M, reps=40):
+    """Microseconds per torch linear layer (the vendor BLAS) on each verify
+    GEMM shape with M rows, bf16 in and out, weights rotated over copies that
+    exceed the 256 MB Infinity Cache.  A reference for the library's own
+    kernels, not part of the decode step."""
+    hdim = cfg.n_heads * cfg.head_dim
+    roles = [("QKV", cfg.d_model, 3 * hdim), ("O", hdim, cfg.d_model), ("gate/up", cfg.d_model, 2 * cfg.d_ffn),
+             ("down", cfg.d_ffn, cfg.d_model), ("LM head", cfg.d_model, cfg.vocab)]
+    lin = torch.nn.functional.linear  # y = x W^T with W stored [N][K], as a linear layer holds it
+    out = {}
+    for name, K, N in roles:
+        copies = min(8, max(2, int(700e6 // (K * N * 2)) + 1))
+        ws = [torch.randn(N, K, device=dev, dtype=torch.bfloat16) for _ in range(copies)]
+        x = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
+        for i in range(4):
+            y = lin(x, ws[i % copies])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(reps):
+            y = lin(x, ws[i % copies])
+        e1.record()
+        e1.synchronize()
+        out[name] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+        del ws, x, y
+    torch.cuda.empty_cache()
+    return out
 
 
 def counter_traffic():
@@ -404,6 +435,11 @@ def main():
         torch.cuda.synchronize()
         log("[bench] copy calibration: 3 x 1 GiB device copies")
         del src, dst
+    torch_ref = None
+    if a.torch_gemm_reference:
+        rows = B * (len(synth.TREES[wl.tree]) + 1)  # the verify pass's rows: root and tree nodes per sequence
+        torch_ref = {"rows": rows, "us_per_launch": torch_gemm_reference(torch, dev, cfg, rows)}
+        log(f"[bench] torch matmul reference: {torch_ref}")
     cpu = None
     if not a.no_cpu_baseline and B == 1:
         log("[bench] CPU oracle baseline (8 timed oracle steps)")
@@ -505,6 +541,8 @@ def main():
         "speedup_vs_greedy": round(value / ar_rate, 3),
         "cpu_baseline": cpu,
     }
+    if torch_ref:
+        line["torch_gemm_reference"] = torch_ref
     print(json.dumps(line), flush=True)
     spec.close()
     ar.close()
