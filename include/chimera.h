@@ -272,6 +272,25 @@ chimera_status chimera_set_trigram_cache(chimera_ctx* ctx, void* arena, int64_t 
 /* Cumulative draft-level trigram lookups and hits since the cache was attached. */
 chimera_status chimera_trigram_cache_stats(chimera_ctx* ctx, int64_t* lookups, int64_t* hits);
 
+/* DEBUG MODE -- compaction check (race detection for the in-place KV
+ * compaction after acceptance, Sec. 4.3).  While a side arena is attached,
+ * every step copies the K and V rows of all tree nodes (slots n..n+N-1,
+ * every layer and head) into the arena after the verify pass, and after the
+ * compaction compares slot n+d of every sequence and layer with the copy of
+ * the accepted path's node path[d], d = 0..L-1.  The arena (device memory of
+ * chimera_compaction_check_bytes: 256 bytes of counters, then
+ * [layer][K|V][batch][node][heads * head_dim] in the storage type for the
+ * context's maximum batch; 256-byte aligned) is owned by the caller and borrowed until it is detached
+ * (arena == NULL) or the context is freed.  Attaching zeroes the counters
+ * and synchronises the device; attaching or detaching re-captures the step
+ * graph.  CHIMERA_ENOMEM if the arena is too small, CHIMERA_EINVAL if it is
+ * misaligned.  The step's tokens and cache are the same with and without it. */
+chimera_status chimera_compaction_check_bytes(const chimera_ctx* ctx, int64_t* bytes);
+chimera_status chimera_set_compaction_check(chimera_ctx* ctx, void* arena, int64_t arena_bytes);
+/* Rows compared and 16-byte chunks found different since the arena was
+ * attached (synchronises the device).  CHIMERA_ESTATE when no arena is attached. */
+chimera_status chimera_compaction_check_read(chimera_ctx* ctx, int64_t* rows_checked, int64_t* mismatches);
+
 /* TEST HOOK -- allocates.  y[M][N] (float32, host) = x[M][K] @ w[K][N]
  * through the repack and GEMM kernels of `dtype`, on device buffers the call
  * allocates (hipMalloc) and frees itself; synchronises the device.  x and w

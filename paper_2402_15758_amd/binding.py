@@ -75,6 +75,9 @@ _PROTOS = {
     "chimera_set_drafting": [P, I32],
     "chimera_set_trigram_cache": [P, P, I64, I32],
     "chimera_trigram_cache_stats": [P, PI64, PI64],
+    "chimera_compaction_check_bytes": [P, PI64],
+    "chimera_set_compaction_check": [P, P, I64],
+    "chimera_compaction_check_read": [P, PI64, PI64],
 }
 
 
@@ -228,6 +231,22 @@ def chimera_trigram_cache_stats(ctx: int):
     lookups, hits = I64(), I64()
     _check(lib().chimera_trigram_cache_stats(ctx, ctypes.byref(lookups), ctypes.byref(hits)))
     return lookups.value, hits.value
+
+
+def chimera_compaction_check_bytes(ctx: int) -> int:
+    out = I64()
+    _check(lib().chimera_compaction_check_bytes(ctx, ctypes.byref(out)))
+    return out.value
+
+
+def chimera_set_compaction_check(ctx: int, arena_ptr, arena_bytes: int):
+    _check(lib().chimera_set_compaction_check(ctx, arena_ptr, arena_bytes))
+
+
+def chimera_compaction_check_read(ctx: int):
+    rows, bad = I64(), I64()
+    _check(lib().chimera_compaction_check_read(ctx, ctypes.byref(rows), ctypes.byref(bad)))
+    return rows.value, bad.value
 
 
 def chimera_ctx_free(ctx: int):

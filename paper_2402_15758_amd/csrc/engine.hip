@@ -197,6 +197,10 @@ struct chimera_ctx {
   // trigram lookup cache (attached by chimera_set_trigram_cache; hit/miss/stats live in this arena)
   TriCache tri;
   bool tri_on = false;
+  // compaction check (debug mode): counters then the tree K/V copy, in a
+  // caller-owned arena; nullptr = off
+  unsigned long long* cc_counts = nullptr;
+  void* cc_side = nullptr;
   // decoding: greedy, or typical acceptance with sampling (chimera_set_decoding)
   int typical = 0;
   float temperature = 1.f, t_eps = 0.09f, t_delta = 0.3f;
@@ -1262,7 +1266,10 @@ void enqueue_step(chimera_ctx* ctx, hipStream_t st) {
       launch_argmax(ctx->logits, M, V, ctx->amax, q);
     mark(2, q);
     launch_accept(dt, s, q);
+    if (ctx->cc_side) launch_kv_snapshot(dt, s, kv->pool, cf.n_layers, kv->layer_stride, ctx->cc_side, q);
     launch_compact(dt, s, kv->pool, cf.n_layers, kv->layer_stride, q);
+    if (ctx->cc_side)
+      launch_kv_check(dt, s, kv->pool, cf.n_layers, kv->layer_stride, ctx->cc_side, ctx->cc_counts, q);
     launch_advance(dt, s, q);
     mark(3, q);
   };
@@ -1727,6 +1734,49 @@ chimera_status chimera_set_trigram_cache(chimera_ctx* ctx, void* arena, int64_t 
     HIPCK(hipMemset(ctx->tri.stats, 0, 2 * sizeof(unsigned long long)));
     HIPCK(hipDeviceSynchronize());
     ctx->tri_on = true;
+  });
+}
+
+chimera_status chimera_compaction_check_bytes(const chimera_ctx* ctx, int64_t* bytes) {
+  return guard([&] {
+    check_ctx(const_cast<chimera_ctx*>(ctx));
+    REQUIRE(bytes != nullptr, CHIMERA_EINVAL, "null argument");
+    const chimera_config& cf = ctx->m->cfg;
+    // sized for the context's maximum batch, so any prefill batch fits
+    *bytes = 256 + (int64_t)cf.n_layers * 2 * ctx->B * ctx->N * cf.n_heads * cf.head_dim * ctx->m->es;
+  });
+}
+
+chimera_status chimera_set_compaction_check(chimera_ctx* ctx, void* arena, int64_t arena_bytes) {
+  return guard([&] {
+    check_ctx(ctx);
+    drop_graph(ctx);
+    if (arena == nullptr) {
+      ctx->cc_side = nullptr;
+      ctx->cc_counts = nullptr;
+      return;
+    }
+    int64_t need = 0;
+    chimera_compaction_check_bytes(ctx, &need);
+    REQUIRE(arena_bytes >= need, CHIMERA_ENOMEM, "compaction check arena too small");
+    REQUIRE(((uintptr_t)arena & 255) == 0, CHIMERA_EINVAL, "arena must be 256-byte aligned");
+    HIPCK(hipMemset(arena, 0, 256));  // the counters
+    HIPCK(hipDeviceSynchronize());
+    ctx->cc_counts = (unsigned long long*)arena;
+    ctx->cc_side = (char*)arena + 256;
+  });
+}
+
+chimera_status chimera_compaction_check_read(chimera_ctx* ctx, int64_t* rows_checked, int64_t* mismatches) {
+  return guard([&] {
+    check_ctx(ctx);
+    REQUIRE(rows_checked != nullptr && mismatches != nullptr, CHIMERA_EINVAL, "null argument");
+    REQUIRE(ctx->cc_counts != nullptr, CHIMERA_ESTATE, "compaction check is not enabled");
+    unsigned long long c[2] = {0, 0};
+    HIPCK(hipDeviceSynchronize());
+    HIPCK(hipMemcpy(c, ctx->cc_counts, sizeof(c), hipMemcpyDeviceToHost));
+    *rows_checked = (int64_t)c[0];
+    *mismatches = (int64_t)c[1];
   });
 }
 

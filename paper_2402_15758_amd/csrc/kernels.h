@@ -226,6 +226,13 @@ void launch_topk(const float* logits, int64_t ld, const StepState& s, const Draf
 void launch_tree_setup(const StepState& s, hipStream_t st);
 void launch_accept(int dtype, const StepState& s, hipStream_t st);
 void launch_compact(int dtype, const StepState& s, void* pool, int n_layers, int64_t layer_stride, hipStream_t st);
+// Compaction check: the tree's K/V rows of every layer copied to side
+// [layer][kv][B][N][H*hd] before compaction, compared with the accepted
+// path's slots after it (counts[0] += rows, counts[1] += differing chunks).
+void launch_kv_snapshot(int dtype, const StepState& s, const void* pool, int n_layers, int64_t layer_stride,
+                        void* side, hipStream_t st);
+void launch_kv_check(int dtype, const StepState& s, const void* pool, int n_layers, int64_t layer_stride,
+                     const void* side, unsigned long long* counts, hipStream_t st);
 void launch_advance(int dtype, const StepState& s, hipStream_t st);
 
 // Rows of draft level lv.  Rows [0, B R) are the queries (trigram position

@@ -593,6 +593,66 @@ __global__ __launch_bounds__(256) void compact_kernel(StepState s, T* pool, int6
   }
 }
 
+// Compaction check (debug mode).  Before compaction: node u's K or V row of
+// every layer (slot n+u, all heads) is copied to
+// side[((layer * 2 + kv) * B + b) * N + u][H * hd].  After compaction: slot
+// n+d must hold the copy of node path[d] for d = 0..L-1; counts[0] gains the
+// rows compared and counts[1] the 16-byte chunks that differ.
+template <typename T>
+__global__ __launch_bounds__(256) void kv_snapshot_kernel(StepState s, const T* pool, int64_t layer_stride,
+                                                          T* side) {
+  const int layer = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  const int n = s.n[b];
+  constexpr int VEC = ET<T>::VEC;
+  const T* base = pool + (int64_t)layer * layer_stride + (int64_t)kv * s.H * s.ps * s.hd;
+  const int* ptab = s.page_table + (int64_t)b * s.max_pages;
+  const int nvec = s.H * s.hd / VEC;
+  T* dst = side + (((int64_t)layer * 2 + kv) * s.B + b) * s.N * s.H * s.hd;
+  for (int u = 0; u < s.N; ++u) {
+    const int slot = n + u;
+    const int64_t sb = (int64_t)ptab[slot / s.ps] * s.page_stride + (int64_t)(slot % s.ps) * s.hd;
+    for (int e = threadIdx.x; e < nvec; e += 256) {
+      const int h = (e * VEC) / s.hd, dim = (e * VEC) % s.hd;
+      st16(dst + (int64_t)u * s.H * s.hd + e * VEC, ld16(base + sb + (int64_t)h * s.ps * s.hd + dim));
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void kv_check_kernel(StepState s, const T* pool, int64_t layer_stride,
+                                                       const T* side, unsigned long long* counts) {
+  __shared__ unsigned int bad;
+  const int layer = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  const int L = s.out_len[b];
+  const int n = s.n[b];
+  const int K1 = s.K + 1;
+  constexpr int VEC = ET<T>::VEC;
+  const T* base = pool + (int64_t)layer * layer_stride + (int64_t)kv * s.H * s.ps * s.hd;
+  const int* ptab = s.page_table + (int64_t)b * s.max_pages;
+  const int nvec = s.H * s.hd / VEC;
+  const T* snap = side + (((int64_t)layer * 2 + kv) * s.B + b) * s.N * s.H * s.hd;
+  if (threadIdx.x == 0) bad = 0;
+  __syncthreads();
+  unsigned int mine = 0;
+  for (int dd = 0; dd < L; ++dd) {
+    const int u = s.out_nodes[b * K1 + dd];
+    const int slot = n + dd;
+    const int64_t db = (int64_t)ptab[slot / s.ps] * s.page_stride + (int64_t)(slot % s.ps) * s.hd;
+    for (int e = threadIdx.x; e < nvec; e += 256) {
+      const int h = (e * VEC) / s.hd, dim = (e * VEC) % s.hd;
+      const int4 got = ld16(base + db + (int64_t)h * s.ps * s.hd + dim);
+      const int4 want = ld16(snap + (int64_t)u * s.H * s.hd + e * VEC);
+      mine += (got.x != want.x || got.y != want.y || got.z != want.z || got.w != want.w) ? 1u : 0u;
+    }
+  }
+  if (mine) atomicAdd(&bad, mine);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    atomicAdd(&counts[0], (unsigned long long)L);
+    if (bad) atomicAdd(&counts[1], (unsigned long long)bad);
+  }
+}
+
 // Workgroup (b, idx) moves accepted row idx of sequence b into the encoder
 // prologue rows (and h_last for the last one); workgroup (b, 0) also commits
 // the tokens and advances n.
@@ -953,6 +1013,26 @@ void launch_compact(int dtype, const StepState& s, void* pool, int n_layers, int
   else
     hipLaunchKernelGGL(compact_kernel<float>, dim3(n_layers, 2, s.B), dim3(256), 0, st, s, (float*)pool,
                        layer_stride);
+}
+
+void launch_kv_snapshot(int dtype, const StepState& s, const void* pool, int n_layers, int64_t layer_stride,
+                        void* side, hipStream_t st) {
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(kv_snapshot_kernel<bf16_t>, dim3(n_layers, 2, s.B), dim3(256), 0, st, s, (const bf16_t*)pool,
+                       layer_stride, (bf16_t*)side);
+  else
+    hipLaunchKernelGGL(kv_snapshot_kernel<float>, dim3(n_layers, 2, s.B), dim3(256), 0, st, s, (const float*)pool,
+                       layer_stride, (float*)side);
+}
+
+void launch_kv_check(int dtype, const StepState& s, const void* pool, int n_layers, int64_t layer_stride,
+                     const void* side, unsigned long long* counts, hipStream_t st) {
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(kv_check_kernel<bf16_t>, dim3(n_layers, 2, s.B), dim3(256), 0, st, s, (const bf16_t*)pool,
+                       layer_stride, (const bf16_t*)side, counts);
+  else
+    hipLaunchKernelGGL(kv_check_kernel<float>, dim3(n_layers, 2, s.B), dim3(256), 0, st, s, (const float*)pool,
+                       layer_stride, (const float*)side, counts);
 }
 
 void launch_advance(int dtype, const StepState& s, hipStream_t st) {

@@ -193,6 +193,24 @@ class Session:
         """(lookups, hits) of draft-level trigram rows since the cache was attached."""
         return B.chimera_trigram_cache_stats(self.ctx)
 
+    def compaction_check(self, enable: bool):
+        """Attach (or detach) the compaction check's side arena: every step then
+        copies the tree's K/V rows before compaction and compares the accepted
+        path's slots with them after it."""
+        import torch
+        if not enable:
+            B.chimera_set_compaction_check(self.ctx, None, 0)
+            self.cc_arena = None
+            return
+        nb = B.chimera_compaction_check_bytes(self.ctx)
+        self.cc_arena = torch.empty(nb + 256, dtype=torch.uint8, device=self.device)
+        base = (self.cc_arena.data_ptr() + 255) // 256 * 256
+        B.chimera_set_compaction_check(self.ctx, base, nb)
+
+    def compaction_check_read(self):
+        """(rows compared, 16-byte chunks that differed) since the check was attached."""
+        return B.chimera_compaction_check_read(self.ctx)
+
     def profile(self, enable: bool):
         B.chimera_profile_enable(self.ctx, enable)
 
@@ -202,6 +220,7 @@ class Session:
     def close(self):
         if getattr(self, "ctx", None):
             B.chimera_set_trigram_cache(self.ctx, None, 0, 0)
+            B.chimera_set_compaction_check(self.ctx, None, 0)
             B.chimera_ctx_free(self.ctx)
             self.ctx = None
         if getattr(self, "kv", None):
