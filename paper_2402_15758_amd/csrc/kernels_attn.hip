@@ -71,7 +71,9 @@ __global__ void attn_rows_kernel(const int* __restrict__ n_b, const int* __restr
 // 16w .. 16w+15 as MFMA columns.  S^T = K Q^T, then O^T += V^T P^T.
 // ---------------------------------------------------------------------------
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
+// Three waves per SIMD (168 VGPRs or fewer): the pass is bound by the issue
+// of its per-chunk VALU and MFMA chains, so occupancy is what hides them.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void tree_attn_shared(const TreeAttnArgs a) {
   constexpr int VEC = ET<T>::VEC, KB = 4 * VEC;
   constexpr int KP = HD + VEC;         // K row pitch (elements)
   constexpr int VP = CHUNK + VEC;      // V^T row pitch (elements)
@@ -151,13 +153,15 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
   load_chunk(c_begin);
   for (int c = c_begin; c <= c_end; ++c) {
     __syncthreads();
+    // every row of the chunk written so far: no zero staging (uniform)
+    const bool whole = (c + 1) * CHUNK <= wlim;
 #pragma unroll
     for (int t = 0; t < PER; ++t) {
       const int idx = tid + 256 * t;
       const int4 zero = int4{0, 0, 0, 0};
-      st16(&Ks[(idx / PARTS) * KP + (idx % PARTS) * VEC], c * CHUNK + idx / PARTS < wlim ? kreg[t] : zero);
+      st16(&Ks[(idx / PARTS) * KP + (idx % PARTS) * VEC], whole || c * CHUNK + idx / PARTS < wlim ? kreg[t] : zero);
       const int key = idx % CHUNK, part = idx / CHUNK;
-      const int4 vk = c * CHUNK + key < wlim ? vreg[t] : zero;
+      const int4 vk = whole || c * CHUNK + key < wlim ? vreg[t] : zero;
       if constexpr (sizeof(T) == 2) {
         // V^T as 32-bit words holding keys (2j, 2j+1): the two lanes (same
         // wave) swap half of their 8 dims, then the even lane writes dims
@@ -191,32 +195,58 @@ __global__ __launch_bounds__(256) void tree_attn_shared(const TreeAttnArgs a) {
       for (int ks = 0; ks < HD / KB; ++ks)
         s[kb] = mfma_kb<T>(ld16(&Ks[(16 * kb + c16) * KP + ks * KB + g * VEC]), qf[ks], s[kb]);
     }
+    // When every key of the chunk is visible to every valid query of the
+    // wave (the wave-uniform common case), the masks and the -inf guards
+    // are skipped: the values are the same ones the masked path computes.
+    const bool open = __builtin_amdgcn_ballot_w64(valid_u && c * CHUNK + CHUNK - 1 > lim_u) == 0;
     float mc = -CH_INF;
+    float alpha = 1.f, ls = 0.f, mn;
+    if (open) {
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool act = valid_u && c * CHUNK + 16 * kb + 4 * g + r <= lim_u;  // S^T row = key
-        const float v = act ? s[kb][r] * scale2 : -CH_INF;
-        s[kb][r] = v;
-        mc = fmaxf(mc, v);
-      }
-    mc = rows_max(mc);
-    const float mn = fmaxf(m, mc);
-    float alpha = 1.f, ls = 0.f;
-    if (mn != -CH_INF) {
+        for (int r = 0; r < 4; ++r) {
+          const float v = s[kb][r] * scale2;
+          s[kb][r] = v;
+          mc = fmaxf(mc, v);
+        }
+      mc = rows_max(mc);
+      mn = fmaxf(m, mc);
       alpha = exp2_diff(m, mn);
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = exp2_diff(s[kb][r], mn);
+          const float p = __builtin_amdgcn_exp2f(s[kb][r] - mn);
           s[kb][r] = p;
           ls = ls + p;
         }
     } else {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool act = valid_u && c * CHUNK + 16 * kb + 4 * g + r <= lim_u;  // S^T row = key
+          const float v = act ? s[kb][r] * scale2 : -CH_INF;
+          s[kb][r] = v;
+          mc = fmaxf(mc, v);
+        }
+      mc = rows_max(mc);
+      mn = fmaxf(m, mc);
+      if (mn != -CH_INF) {
+        alpha = exp2_diff(m, mn);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float p = exp2_diff(s[kb][r], mn);
+            s[kb][r] = p;
+            ls = ls + p;
+          }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
     }
     ls = rows_sum(ls);
     l = l * alpha + ls;
