@@ -360,6 +360,10 @@ __global__ __launch_bounds__(256) void tree_attn_window(const TreeAttnArgs a) {
     for (int i = 0; i < NQ; ++i) qv[i] = ld16(qrow + i * VEC);
   }
   float bm[BATCH], bl[BATCH], bo[BATCH][DPL];
+  // this (sequence, head, query)'s partials: group g at slot base + g * N
+  const int64_t slot0 = ((int64_t)b * a.H + h) * a.G * a.N + u;
+  const float* pml = a.part_ml + slot0 * 2;
+  const float* po = a.part_o + slot0 * HD + DPL * lane;
   auto load_batch = [&](int g0, int lim_g) {
 #pragma unroll
     for (int t = 0; t < BATCH; ++t) {
@@ -368,11 +372,11 @@ __global__ __launch_bounds__(256) void tree_attn_window(const TreeAttnArgs a) {
 #pragma unroll
       for (int e = 0; e < DPL; ++e) bo[t][e] = 0.f;
       if (g0 + t < lim_g) {
-        const int64_t slot = (((int64_t)b * a.H + h) * a.G + g0 + t) * a.N + u;
-        bm[t] = a.part_ml[slot * 2];
-        bl[t] = a.part_ml[slot * 2 + 1];
+        const int gs = (g0 + t) * a.N;  // group offset in slots
+        bm[t] = pml[gs * 2];
+        bl[t] = pml[gs * 2 + 1];
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) bo[t][e] = a.part_o[slot * HD + DPL * lane + e];
+        for (int e = 0; e < DPL; ++e) bo[t][e] = po[gs * HD + e];
       }
     }
   };
