@@ -19,8 +19,19 @@ import synth
 from oracle import chimera_oracle as co
 
 
+# Set by the autouse fixture in conftest.py to the test's capsys: progress
+# lines then reach the terminal even while pytest captures output, so a long
+# GPU test shows it is alive between its steps.
+_PROGRESS_SINK = None
+
+
 def log(*a):
-    print(*a, flush=True)
+    sink = _PROGRESS_SINK
+    if sink is not None:
+        with sink.disabled():
+            print(*a, flush=True)
+    else:
+        print(*a, flush=True)
     sys.stdout.flush()
 
 
