@@ -43,6 +43,13 @@ __device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) {
   typedef __bf16 b2 __attribute__((ext_vector_type(2)));
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, b2));
 }
+// gfx950's transposed LDS read of four 16-bit elements (layout described at
+// its use in the shared pass)
+__device__ __forceinline__ int2 ld_tr16(const void* p) {
+  typedef short s4 __attribute__((ext_vector_type(4)));
+  const s4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)p);
+  return __builtin_bit_cast(int2, v);
+}
 __device__ __forceinline__ float exp2_diff(float a, float b) {
   return a == -CH_INF ? 0.0f : __builtin_amdgcn_exp2f(a - b);
 }
@@ -75,11 +82,15 @@ template <typename T, int HD>
 // of its per-chunk VALU and MFMA chains, so occupancy is what hides them.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void tree_attn_shared(const TreeAttnArgs a) {
   constexpr int VEC = ET<T>::VEC, KB = 4 * VEC;
+  constexpr bool B16 = sizeof(T) == 2;
   constexpr int KP = HD + VEC;         // K row pitch (elements)
-  constexpr int VP = CHUNK + VEC;      // V^T row pitch (elements)
-  static_assert(VP % 2 == 0 && CHUNK % 2 == 0, "V^T rows hold whole 32-bit key pairs");
+  // 16-bit V is staged as it lies in the cache, one key per row, and read
+  // back transposed by ds_read_b64_tr_b16; the 16-element pad puts the 16
+  // rows of one transposed read on distinct banks.  fp32 V is staged as V^T.
+  constexpr int VRP = HD + 16;         // V row pitch (16-bit elements)
+  constexpr int VP = CHUNK + VEC;      // V^T row pitch (fp32 elements)
   __shared__ __attribute__((aligned(16))) T Ks[CHUNK * KP];
-  __shared__ __attribute__((aligned(16))) T Vt[HD * VP];
+  __shared__ __attribute__((aligned(16))) T Vt[B16 ? CHUNK * VRP : HD * VP];
 
   __shared__ int64_t pbase[GMAX * CHUNK];  // element offset of each staged key's row
   const int grp = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -136,18 +147,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) voi
   // chunk c+1 are issued before chunk c is reduced.
   constexpr int PER = CHUNK * (HD / VEC) / 256;
   int4 kreg[PER], vreg[PER];
-  // K: consecutive lanes read consecutive 16-byte parts of a row (whole
-  // rows per instruction); V: consecutive lanes read the same part of
-  // consecutive rows, the order its transposed LDS writes need
+  // Consecutive lanes read consecutive 16-byte parts of a row (whole rows
+  // per instruction), except fp32 V: there consecutive lanes read the same
+  // part of consecutive rows, the order its transposed LDS writes need.
   constexpr int PARTS = HD / VEC;
+  auto v_key = [](int idx) { return B16 ? idx / PARTS : idx % CHUNK; };
+  auto v_part = [](int idx) { return B16 ? idx % PARTS : idx / CHUNK; };
   auto load_chunk = [&](int c) {
 #pragma unroll
     for (int t = 0; t < PER; ++t) {
       const int idx = tid + 256 * t;
       const int kk = idx / PARTS, kp = idx % PARTS;
       kreg[t] = ld16(kpool + pbase[(c - c_begin) * CHUNK + kk] + kp * VEC);
-      const int key = idx % CHUNK, part = idx / CHUNK;
-      vreg[t] = ld16(vpool + pbase[(c - c_begin) * CHUNK + key] + part * VEC);
+      vreg[t] = ld16(vpool + pbase[(c - c_begin) * CHUNK + v_key(idx)] + v_part(idx) * VEC);
     }
   };
   load_chunk(c_begin);
@@ -160,23 +172,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) voi
       const int idx = tid + 256 * t;
       const int4 zero = int4{0, 0, 0, 0};
       st16(&Ks[(idx / PARTS) * KP + (idx % PARTS) * VEC], whole || c * CHUNK + idx / PARTS < wlim ? kreg[t] : zero);
-      const int key = idx % CHUNK, part = idx / CHUNK;
+      const int key = v_key(idx), part = v_part(idx);
       const int4 vk = whole || c * CHUNK + key < wlim ? vreg[t] : zero;
-      if constexpr (sizeof(T) == 2) {
-        // V^T as 32-bit words holding keys (2j, 2j+1): the two lanes (same
-        // wave) swap half of their 8 dims, then the even lane writes dims
-        // 0-3 and the odd lane dims 4-7
-        const bool odd = key & 1;
-        const uint32_t r0 = __builtin_amdgcn_update_dpp(0, odd ? vk.x : vk.z, DPP_XOR1, 0xF, 0xF, false);
-        const uint32_t r1 = __builtin_amdgcn_update_dpp(0, odd ? vk.y : vk.w, DPP_XOR1, 0xF, 0xF, false);
-        const uint32_t m0 = odd ? vk.z : vk.x, m1 = odd ? vk.w : vk.y;  // own dims, two per word
-        const uint32_t lo0 = odd ? r0 : m0, hi0 = odd ? m0 : r0;        // key 2j, key 2j+1
-        const uint32_t lo1 = odd ? r1 : m1, hi1 = odd ? m1 : r1;
-        uint32_t* vw = reinterpret_cast<uint32_t*>(Vt) + ((part * VEC + (odd ? 4 : 0)) * VP + (key & ~1)) / 2;
-        vw[0] = (lo0 & 0xffffu) | (hi0 << 16);
-        vw[VP / 2] = (lo0 >> 16) | (hi0 & 0xffff0000u);
-        vw[VP] = (lo1 & 0xffffu) | (hi1 << 16);
-        vw[3 * VP / 2] = (lo1 >> 16) | (hi1 & 0xffff0000u);
+      if constexpr (B16) {
+        st16(&Vt[key * VRP + part * VEC], vk);
       } else {
         const T* ve = reinterpret_cast<const T*>(&vk);
 #pragma unroll
@@ -276,15 +275,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) voi
         const int4 mfrag = int4{(int)pm[0], (int)pm[1], (int)pm[2], (int)pm[3]};
         const int4 lfrag = int4{(int)pl[0], (int)pl[1], (int)pl[2], (int)pl[3]};
         // V^T fragments two output blocks at a time; within a pair the terms
-        // alternate between the two accumulators
+        // alternate between the two accumulators.  Lane (g, c16) needs dim
+        // 16 db + c16 of keys 32 kp + 4 g + {0..3} and 32 kp + 16 + 4 g +
+        // {0..3}, the key order of the P fragment.  A transposed read hands
+        // lane i of each 16-lane group element i % 4 of the 8-byte blocks
+        // addressed by lanes i / 4 + 4 e (e = 0..3), so lane (g, c16)
+        // addresses row 32 kp + 4 g + c16 / 4 (plus 16 for the second half),
+        // dims 16 db + 4 (c16 % 4) .. + 3.
+        const T* vrow = &Vt[(32 * kp + 4 * g + (c16 >> 2)) * VRP + 4 * (c16 & 3)];
 #pragma unroll
         for (int d2 = 0; d2 < HD / 16; d2 += 2) {
           int4 vf[2];
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
-            const T* vr = &Vt[(16 * (d2 + j) + c16) * VP];
-            const int2 lo = *reinterpret_cast<const int2*>(vr + 32 * kp + 4 * g);
-            const int2 hi = *reinterpret_cast<const int2*>(vr + 32 * kp + 16 + 4 * g);
+            const int2 lo = ld_tr16(vrow + 16 * (d2 + j));
+            const int2 hi = ld_tr16(vrow + 16 * VRP + 16 * (d2 + j));
             vf[j] = int4{lo.x, lo.y, hi.x, hi.y};
           }
           o[d2] = mfma_kb<T>(vf[0], hfrag, o[d2]);
