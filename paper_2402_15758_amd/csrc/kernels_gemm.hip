@@ -210,30 +210,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
                                               const f32x4 (&acc)[MB][CB], f32x4* red, const RowMeta* rm,
                                               float* stage, int wave, int lane, int split) {
   const int g = lane >> 4, c16 = lane & 15;
-#pragma unroll
-  for (int i = 0; i < MB; ++i)
-#pragma unroll
-    for (int jj = 0; jj < JN; ++jj) red[((wave * MB + i) * JN + jj) * 64 + lane] = acc[i][J0 + jj];
-  __syncthreads();
   // this wave's output tiles: items it = wave, wave + 4, ... of MB * JN
   constexpr int ITEMS = (MB * JN + 3) / 4;
-  f32x4 vv[ITEMS], vpp[ITEMS];
-#pragma unroll
-  for (int k = 0; k < ITEMS; ++k) {
-    const int it = wave + 4 * k;
-    if (it < MB * JN) {  // wave-uniform
-      const int i = it / JN, j = it % JN;
-      f32x4 v = red[((0 * MB + i) * JN + j) * 64 + lane];
-#pragma unroll
-      for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * JN + j) * 64 + lane];
-      vv[k] = v;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) vpp[k][r] = dpp_mov<DPP_ROR8>(v[r]);  // lane column c16 ^ 8
-    }
-  }
+  // QKV: the rotary table entries of every element are requested first, so
+  // that their round trip overlaps the reduction below
+  float cs[ITEMS][4], sn[ITEMS][4];
   if (kind == EPI_QKV) {
-    // rotary tables for every element first, then the stores
-    float cs[ITEMS][4], sn[ITEMS][4];
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
       const int it = wave + 4 * k;
@@ -253,6 +235,27 @@ __device__ __forceinline__ void gemm_epilogue(const GemmShape& sh, const GemmEpi
         }
       }
     }
+  }
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int jj = 0; jj < JN; ++jj) red[((wave * MB + i) * JN + jj) * 64 + lane] = acc[i][J0 + jj];
+  __syncthreads();
+  f32x4 vv[ITEMS], vpp[ITEMS];
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const int it = wave + 4 * k;
+    if (it < MB * JN) {  // wave-uniform
+      const int i = it / JN, j = it % JN;
+      f32x4 v = red[((0 * MB + i) * JN + j) * 64 + lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v = v + red[((w * MB + i) * JN + j) * 64 + lane];
+      vv[k] = v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vpp[k][r] = dpp_mov<DPP_ROR8>(v[r]);  // lane column c16 ^ 8
+    }
+  }
+  if (kind == EPI_QKV) {
     if constexpr (sizeof(T) == 2) {
       // each 16x16 tile goes through the wave's LDS tile, then 32 lanes store
       // 8 consecutive outputs of one row each
