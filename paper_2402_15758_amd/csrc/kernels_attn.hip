@@ -143,7 +143,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) voi
 
   const T* kpool = (const T*)a.kpool;
   const T* vpool = (const T*)a.vpool;
-  // K rows and V^T of one chunk pass through registers: the global loads of
+  // K and V rows of one chunk pass through registers: the global loads of
   // chunk c+1 are issued before chunk c is reduced.
   constexpr int PER = CHUNK * (HD / VEC) / 256;
   int4 kreg[PER], vreg[PER];
