@@ -5,7 +5,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_helpers import TieLog, check_step, compare_lists, gpu_step, log, make_session, tau, used_lists
+from gpu_helpers import (TieLog, check_step, compare_lists, gpu_step, log, make_session, tau,
+                         teacher_forced_config, used_lists)
 from oracle import chimera_oracle as co
 
 pytestmark = pytest.mark.gpu
@@ -663,3 +664,25 @@ def test_wide_batch_teacher_forced():
             check_step(art, b, decs[b], tau(WIDE_CFG), ties)
     log(f"ties: argmax {ties.argmax_ties}, lists {ties.list_ties}")
     sp.close()
+
+
+# ---------------------------------------------------------------------------
+# bf16 with heads of 64: the library's other 16-bit attention instantiation
+# (tree and encoder attention at head_dim 64, whose staged V rows and
+# transposed LDS reads use a different row pitch than at head_dim 128)
+# ---------------------------------------------------------------------------
+HD64_CFG = synth.small_config(n_layers=2, d_model=256, n_heads=4, head_dim=64, d_ffn=512, vocab=2048,
+                              n_draft_heads=4)
+
+
+def test_bf16_head_dim_64_teacher_forced():
+    """Two ragged sequences, one short and one past position 1024 (so the
+    shared pass runs near pairs, far groups of four and a partial last
+    chunk), T32 with per-sequence forcing, node by node against the float64
+    oracle."""
+    w = synth.make_weights(HD64_CFG, std=0.06, device="cpu")
+    prompts = [synth.make_prompt(n, HD64_CFG.vocab, 1300 + n) for n in (70, 1109)]
+    err, _, lens = teacher_forced_config(HD64_CFG, w, prompts, synth.TREE_T32, [0.6, 0.9], 6,
+                                         compute=np.float64, label="bf16 head_dim 64")
+    assert err <= tau(HD64_CFG)
+    assert max(lens) > 1
