@@ -686,3 +686,18 @@ def test_bf16_head_dim_64_teacher_forced():
                                          compute=np.float64, label="bf16 head_dim 64")
     assert err <= tau(HD64_CFG)
     assert max(lens) > 1
+
+
+# fp32 with heads of 128: the remaining attention instantiation (fp32 V
+# staged as V^T), at the float tolerance
+F32_HD128_CFG = synth.small_config(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=512, vocab=2048,
+                                   n_draft_heads=4, dtype="f32")
+
+
+def test_f32_head_dim_128_teacher_forced():
+    w = synth.make_weights(F32_HD128_CFG, std=0.06, device="cpu")
+    prompts = [synth.make_prompt(n, F32_HD128_CFG.vocab, 1400 + n) for n in (70, 1109)]
+    err, _, lens = teacher_forced_config(F32_HD128_CFG, w, prompts, synth.TREE_T32, [0.6, 0.9], 6,
+                                         compute=np.float64, label="f32 head_dim 128")
+    assert err <= tau(F32_HD128_CFG)
+    assert max(lens) > 1
