@@ -4,7 +4,9 @@
   padding reaches the draft and the encoder memory), the first and last
   vocabulary ids, the largest candidate lists (rank 7, s = 8), decoding up
   to the KV capacity.
-* Paged KV with page sizes 1, 8, 32 and 256 in shuffled page order.
+* Paged KV with page sizes 1, 8, 32 and 256 in shuffled page order; for bf16
+  with heads of 128, page sizes 1, 8, 64 and 256 leave every token and every
+  committed K/V bit as they are with 16-token pages in order.
 * Errors: every invalid call returns its status before any launch and
   leaves the decode state as it was; the following steps equal those of a
   session that never saw the invalid call.
@@ -214,3 +216,50 @@ def test_attention_boundaries(tiny):
             check_step(gpu_step(sess), 0, dec, tau(CFG), ties)
         assert ties.argmax_ties == 0 and ties.list_ties == 0, n0
         sess.close()
+
+
+SMALL_BF16 = synth.small_config(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=512, vocab=2048,
+                                n_draft_heads=4)
+
+
+@pytest.fixture(scope="module")
+def small_bf16_greedy():
+    """GPU greedy stream and committed target K/V of one 600-token prompt,
+    16-token pages in order."""
+    from paper_2402_15758_amd import Session
+    w = synth.make_weights(SMALL_BF16, device="cpu", std=0.06)
+    prompt = synth.make_prompt(600, SMALL_BF16.vocab, 41)
+    ar = Session(SMALL_BF16, w, (), max_len=768)
+    out, _ = ar.generate([prompt], 68)
+    n = int(ar.debug(4)[0])
+    kv = [ar.kv_read(layer, 0, 0, n) for layer in range(SMALL_BF16.n_layers)]
+    ar.close()
+    return w, prompt, out[0], kv, n
+
+
+@pytest.mark.parametrize("page_size", [1, 8, 64, 256])
+def test_bf16_page_sizes_equal_greedy_bitexact(small_bf16_greedy, page_size):
+    """Speculative steps (T64, forced p = 0.7) over shuffled pages of another
+    size: the same tokens as greedy decoding, and the same K/V bits at every
+    committed position of every layer (paging moves rows, never arithmetic)."""
+    import torch
+    from paper_2402_15758_amd import Session
+    w, prompt, ar_out, ar_kv, ar_n = small_bf16_greedy
+    log(f"edges: bf16 page size {page_size}, shuffled pages, forced p = 0.7, against GPU greedy")
+    n0, max_len, G = len(prompt), 768, 60
+    stride = max_len + 8
+    ref = np.full((1, stride), -1, dtype=np.int32)
+    ref[0, n0:n0 + len(ar_out)] = ar_out
+    ok = synth.force_table(0.7, 3, 0, stride)[None]
+    n_pages = int(np.ceil((max_len + 64) / page_size))
+    order = np.random.default_rng(100 + page_size).permutation(n_pages).astype(np.int32)
+    sess = Session(SMALL_BF16, w, synth.TREE_T64, max_len=max_len, page_size=page_size, page_order=order)
+    sess.set_forcing(torch.from_numpy(ref).cuda(), torch.from_numpy(ok).cuda())
+    out, steps = sess.generate([prompt], G)
+    assert out[0] == list(ar_out[:G])
+    assert max(int(nn[0]) for _, nn, _ in steps) > 2
+    n = min(int(sess.debug(4)[0]), ar_n)
+    for layer in range(SMALL_BF16.n_layers):
+        k, v = sess.kv_read(layer, 0, 0, n)
+        assert np.array_equal(k, ar_kv[layer][0][:n]) and np.array_equal(v, ar_kv[layer][1][:n]), layer
+    sess.close()
