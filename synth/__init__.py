@@ -311,4 +311,6 @@ WORKLOADS = {
     "vicuna33b_p512": Workload("vicuna33b_p512", VICUNA33B, "T64", 1, 512, 256, (0.7,)),
     # batch 8, ragged prompts U[256, 2048], T32, p_b ~ U[0.4, 0.9]
     "llama7b_b8": Workload("llama7b_b8", LLAMA7B, "T32", 8, 2048, 128, (0.4, 0.9), prompt_len_lo=256),
+    # the same batch with the 8-node tree: 64 verify rows, as many as one sequence's T64
+    "llama7b_b8_t8": Workload("llama7b_b8_t8", LLAMA7B, "T8", 8, 2048, 128, (0.4, 0.9), prompt_len_lo=256),
 }

@@ -118,3 +118,7 @@ def test_llama7b_p4096_lossless_and_forced_acceptance(w7b):
 
 def test_llama7b_batch8_ragged_lossless_and_forced_acceptance(w7b):
     forced_lossless_run(CFG, w7b, synth.WORKLOADS["llama7b_b8"], steps=16)
+
+
+def test_llama7b_batch8_ragged_t8_lossless_and_forced_acceptance(w7b):
+    forced_lossless_run(CFG, w7b, synth.WORKLOADS["llama7b_b8_t8"], steps=16)
