@@ -65,6 +65,8 @@ def parse():
                     help="only a short sample for hardware-counter passes: the workload's model and tree, "
                          "64-token prompts, three steps launched kernel by kernel, then three 1 GiB device "
                          "copies (the counters' scale reference); prints no benchmark line")
+    ap.add_argument("--counter-prompt", type=int, default=64,
+                    help="prompt tokens of the counter sample (the attention passes' context)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--no-typical", action="store_true", help="skip the typical-decoding (T = 1) measurement")
@@ -265,7 +267,7 @@ def main():
         # the same verify-pass kernels at the workload's rows (batch x tree
         # nodes); a short context keeps the number of dispatches small
         spec.set_graph(False)
-        spec.prefill([p[:64] for p in prompts])
+        spec.prefill([p[:a.counter_prompt] for p in prompts])
         for _ in range(3):
             spec.step()
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
@@ -273,7 +275,8 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-        log(f"[bench] counter sample: {wl.name}, {B} x 64-token prompts, 3 eager steps, 3 x 1 GiB copies")
+        log(f"[bench] counter sample: {wl.name}, {B} x {a.counter_prompt}-token prompts, 3 eager steps, "
+            "3 x 1 GiB copies")
         spec.close()
         return
     ar = Session(cfg, None, (), max_batch=B, max_len=max_len, share_model=spec)

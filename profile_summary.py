@@ -23,8 +23,14 @@ step is told from a plain greedy one by its verify GEMMs covering more than one
 16-row tile block.  The byte counters are scaled by what they read for the
 sample's three 1 GiB device copies (2^20 KiB read and 2^20 KiB written).
 
+  attn      rocprofv3 --pmc <ATTN_COUNTERS> --output-format csv -d DIR -o run --
+                python3 bench.py --workload WL --counter-sample --counter-prompt P
+            -> profiles/attn_counters_WL.md: instruction mix of the verify
+               pass's two tree-attention kernels per dispatch.
+
 usage: python profile_summary.py trace DIR WORKLOAD WARMUP STEPS "COMMAND"
        python profile_summary.py counters DIR WORKLOAD "FETCH_CMD" "WRITE_CMD" "SQ_CMD"
+       python profile_summary.py attn DIR WORKLOAD "COMMAND"
 """
 from __future__ import annotations
 
@@ -313,10 +319,64 @@ def counters(d, wl_name, cmd_f, cmd_w, cmd_sq):
     print("".join(out))
 
 
+# --------------------------------------------------------------------------
+ATTN_COUNTERS = ["SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS",
+                 "SQ_INSTS_SALU", "SQ_LDS_BANK_CONFLICT", "GRBM_GUI_ACTIVE"]
+ATTN_KERNELS = ["tree_attn_shared", "tree_attn_window"]
+
+
+def attn(d, wl_name, cmd):
+    """Instruction mix of the verify pass's tree-attention kernels (the
+    dispatches between each step's verify stamps)."""
+    ds = load_counters(os.path.join(d, "run_counter_collection.csv"))
+    st = [i for i, e in enumerate(ds) if "stamp_kernel" in e["name"]]
+    per = {k: [] for k in ATTN_KERNELS}
+    for g in (st[i:i + 4] for i in range(0, len(st) - 3, 4)):
+        for i in range(g[1] + 1, g[2]):
+            for k in ATTN_KERNELS:
+                if k in ds[i]["name"]:
+                    per[k].append(ds[i])
+    if not per["tree_attn_shared"]:
+        raise SystemExit("no verify-pass attention dispatches between step stamps")
+    mean = lambda rows, c: statistics.mean(r[c] for r in rows)
+    out = [f"# Tree attention instruction mix, workload `{wl_name}` — rocprofv3 --pmc summary\n\n",
+           "One MI355X (gfx950). The verify pass's two attention kernels (shared MFMA pass over 64-position "
+           "chunks, per-query window pass) in the counter sample of `bench.py` (the workload's model and "
+           "tree, the given prompt length, three steps launched kernel by kernel). Made by\n\n"
+           f"```\n{cmd}\npython profile_summary.py attn <DIR> {wl_name} \"<command>\"\n```\n\n"
+           "- counts are rocprofv3's per-dispatch totals over all waves; per-wave figures divide by SQ_WAVES\n"
+           "- a shared-pass wave issues exactly 64 MFMAs per 64-key chunk (16 for S^T = K Q^T, 48 for the "
+           "three-term P V), so SQ_INSTS_MFMA / 64 counts (chunk, wave) pairs and the instructions per 64 "
+           "MFMAs are those of one chunk of one wave, with the pass's prologue and epilogue spread over its "
+           "chunks\n"
+           "- LDS bank conflicts are SQ_LDS_BANK_CONFLICT cycles per LDS instruction\n\n"
+           "| kernel | dispatches | dur us | waves | VALU / wave | MFMA / wave | LDS / wave | SALU / wave | "
+           "VALU per 64 MFMA | LDS per 64 MFMA | conflict cycles / LDS instr |\n"
+           "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|\n"]
+    for k in ATTN_KERNELS:
+        rows = per[k]
+        if not rows:
+            continue
+        waves = mean(rows, "SQ_WAVES")
+        valu, mfma = mean(rows, "SQ_INSTS_VALU"), mean(rows, "SQ_INSTS_MFMA")
+        lds, salu = mean(rows, "SQ_INSTS_LDS"), mean(rows, "SQ_INSTS_SALU")
+        conf = mean(rows, "SQ_LDS_BANK_CONFLICT")
+        dur = statistics.mean(r["dur"] for r in rows) / 1e3
+        chunk = f"{64 * valu / mfma:.0f}" if mfma > 0 else "–"
+        lchunk = f"{64 * lds / mfma:.1f}" if mfma > 0 else "–"
+        out.append(f"| `{k}` | {len(rows)} | {dur:.2f} | {waves:.0f} | {valu / waves:.1f} | {mfma / waves:.1f} | "
+                   f"{lds / waves:.1f} | {salu / waves:.1f} | {chunk} | {lchunk} | "
+                   f"{conf / lds if lds else 0:.3f} |\n")
+    open(os.path.join(OUT_DIR, f"attn_counters_{wl_name}.md"), "w").write("".join(out))
+    print("".join(out))
+
+
 if __name__ == "__main__":
     if len(sys.argv) >= 7 and sys.argv[1] == "trace":
         trace(sys.argv[2], sys.argv[3], int(sys.argv[4]), int(sys.argv[5]), sys.argv[6])
     elif len(sys.argv) >= 7 and sys.argv[1] == "counters":
         counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6])
+    elif len(sys.argv) >= 5 and sys.argv[1] == "attn":
+        attn(sys.argv[2], sys.argv[3], sys.argv[4])
     else:
         raise SystemExit(__doc__)
