@@ -23,14 +23,16 @@ step is told from a plain greedy one by its verify GEMMs covering more than one
 16-row tile block.  The byte counters are scaled by what they read for the
 sample's three 1 GiB device copies (2^20 KiB read and 2^20 KiB written).
 
-  attn      rocprofv3 --pmc <ATTN_COUNTERS> --output-format csv -d DIR -o run --
+  attn      rocprofv3 --pmc <counters> --output-format csv -d DIR/<name> -o run --
                 python3 bench.py --workload WL --counter-sample --counter-prompt P
-            -> profiles/attn_counters_WL.md: instruction mix of the verify
-               pass's two tree-attention kernels per dispatch.
+            for <name> in sq (ATTN_COUNTERS) and optionally fetch (FETCH_SIZE)
+            and write (WRITE_SIZE)
+            -> profiles/attn_counters_WL.md: instruction mix and HBM bytes of
+               the verify pass's two tree-attention kernels per dispatch.
 
 usage: python profile_summary.py trace DIR WORKLOAD WARMUP STEPS "COMMAND"
        python profile_summary.py counters DIR WORKLOAD "FETCH_CMD" "WRITE_CMD" "SQ_CMD"
-       python profile_summary.py attn DIR WORKLOAD "COMMAND"
+       python profile_summary.py attn DIR WORKLOAD "SQ_CMD" ["FETCH_CMD" "WRITE_CMD"]
 """
 from __future__ import annotations
 
@@ -325,25 +327,34 @@ ATTN_COUNTERS = ["SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_INSTS_VALU"
 ATTN_KERNELS = ["tree_attn_shared", "tree_attn_window"]
 
 
-def attn(d, wl_name, cmd):
+def attn(d, wl_name, cmd_sq, cmd_f=None, cmd_w=None):
     """Instruction mix of the verify pass's tree-attention kernels (the
-    dispatches between each step's verify stamps)."""
-    ds = load_counters(os.path.join(d, "run_counter_collection.csv"))
-    st = [i for i, e in enumerate(ds) if "stamp_kernel" in e["name"]]
-    per = {k: [] for k in ATTN_KERNELS}
-    for g in (st[i:i + 4] for i in range(0, len(st) - 3, 4)):
-        for i in range(g[1] + 1, g[2]):
-            for k in ATTN_KERNELS:
-                if k in ds[i]["name"]:
-                    per[k].append(ds[i])
-    if not per["tree_attn_shared"]:
-        raise SystemExit("no verify-pass attention dispatches between step stamps")
+    dispatches between each step's verify stamps) from DIR/sq, and, when
+    DIR/fetch and DIR/write hold FETCH_SIZE and WRITE_SIZE passes of the same
+    sample, their HBM bytes scaled by the sample's 1 GiB copies."""
+
+    def verify_attn(ds):
+        st = [i for i, e in enumerate(ds) if "stamp_kernel" in e["name"]]
+        per = {k: [] for k in ATTN_KERNELS}
+        for g in (st[i:i + 4] for i in range(0, len(st) - 3, 4)):
+            for i in range(g[1] + 1, g[2]):
+                for k in ATTN_KERNELS:
+                    if k in ds[i]["name"]:
+                        per[k].append(ds[i])
+        if not per["tree_attn_shared"]:
+            raise SystemExit("no verify-pass attention dispatches between step stamps")
+        return per
+
+    per = verify_attn(load_counters(os.path.join(d, "sq", "run_counter_collection.csv")))
     mean = lambda rows, c: statistics.mean(r[c] for r in rows)
-    out = [f"# Tree attention instruction mix, workload `{wl_name}` — rocprofv3 --pmc summary\n\n",
+    cmds = "\n".join(c for c in (cmd_sq, cmd_f, cmd_w) if c)
+    args = " ".join(f'"<{n} command>"' for n, c in (("sq", cmd_sq), ("fetch", cmd_f), ("write", cmd_w)) if c)
+    out = [f"# Tree attention counters, workload `{wl_name}` — rocprofv3 --pmc summary\n\n",
            "One MI355X (gfx950). The verify pass's two attention kernels (shared MFMA pass over 64-position "
            "chunks, per-query window pass) in the counter sample of `bench.py` (the workload's model and "
-           "tree, the given prompt length, three steps launched kernel by kernel). Made by\n\n"
-           f"```\n{cmd}\npython profile_summary.py attn <DIR> {wl_name} \"<command>\"\n```\n\n"
+           "tree, the given prompt length, three steps launched kernel by kernel, then three 1 GiB device "
+           "copies). Made by\n\n"
+           f"```\n{cmds}\npython profile_summary.py attn <DIR> {wl_name} {args}\n```\n\n"
            "- counts are rocprofv3's per-dispatch totals over all waves; per-wave figures divide by SQ_WAVES\n"
            "- a shared-pass wave issues exactly 64 MFMAs per 64-key chunk (16 for S^T = K Q^T, 48 for the "
            "three-term P V), so SQ_INSTS_MFMA / 64 counts (chunk, wave) pairs and the instructions per 64 "
@@ -367,6 +378,23 @@ def attn(d, wl_name, cmd):
         out.append(f"| `{k}` | {len(rows)} | {dur:.2f} | {waves:.0f} | {valu / waves:.1f} | {mfma / waves:.1f} | "
                    f"{lds / waves:.1f} | {salu / waves:.1f} | {chunk} | {lchunk} | "
                    f"{conf / lds if lds else 0:.3f} |\n")
+    if cmd_f and cmd_w:
+        fd = load_counters(os.path.join(d, "fetch", "run_counter_collection.csv"))
+        wd = load_counters(os.path.join(d, "write", "run_counter_collection.csv"))
+        ff, fc = copy_scale(fd, "FETCH_SIZE")
+        wf, wc = copy_scale(wd, "WRITE_SIZE")
+        pf, pw = verify_attn(fd), verify_attn(wd)
+        out.append(f"\nHBM bytes per dispatch (FETCH_SIZE x {ff:.4f}, WRITE_SIZE x {wf:.4f}, the factors at which "
+                   "the three 1 GiB copies read 1 GiB each way; durations from the fetch pass):\n\n"
+                   "| kernel | dispatches | fetch MB | write MB | dur us | HBM TB/s |\n|---|---:|---:|---:|---:|---:|\n")
+        for k in ATTN_KERNELS:
+            if not pf[k]:
+                continue
+            f = statistics.mean(r["FETCH_SIZE"] for r in pf[k]) * ff * 1024
+            w = statistics.mean(r["WRITE_SIZE"] for r in pw[k]) * wf * 1024
+            dur = statistics.mean(r["dur"] for r in pf[k]) / 1e9
+            out.append(f"| `{k}` | {len(pf[k])} | {f / 1e6:.2f} | {w / 1e6:.2f} | {dur * 1e6:.2f} | "
+                       f"{(f + w) / dur / 1e12:.2f} |\n")
     open(os.path.join(OUT_DIR, f"attn_counters_{wl_name}.md"), "w").write("".join(out))
     print("".join(out))
 
@@ -376,7 +404,7 @@ if __name__ == "__main__":
         trace(sys.argv[2], sys.argv[3], int(sys.argv[4]), int(sys.argv[5]), sys.argv[6])
     elif len(sys.argv) >= 7 and sys.argv[1] == "counters":
         counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6])
-    elif len(sys.argv) >= 5 and sys.argv[1] == "attn":
-        attn(sys.argv[2], sys.argv[3], sys.argv[4])
+    elif len(sys.argv) in (5, 7) and sys.argv[1] == "attn":
+        attn(sys.argv[2], sys.argv[3], *sys.argv[4:])
     else:
         raise SystemExit(__doc__)

@@ -106,8 +106,15 @@ def test_attention_mix_per_64_mfma(tmp_path, monkeypatch):
     for _ in range(2):
         ds += [(STAMP, 64, 1000, base), (STAMP, 64, 1000, base), (shared, 256, 10000, base),
                (window, 256, 6000, dict(base, SQ_INSTS_MFMA=0.0)), (STAMP, 64, 1000, base), (STAMP, 64, 1000, base)]
-    _write(str(tmp_path / "run_counter_collection.csv"), ds)
-    ps.attn(str(tmp_path), "llama7b_p512", "CMD")
+    _write(str(tmp_path / "sq" / "run_counter_collection.csv"), ds)
+    copies = [(COPY, 1 << 20, 200000, {})] * 3
+    fetch = [(n, g, t, {"FETCH_SIZE": 524288.0 if n == COPY else (2048.0 if "attn" in n else 0.0)})
+             for n, g, t, _ in ds + copies]
+    write = [(n, g, t, {"WRITE_SIZE": 1048576.0 if n == COPY else (512.0 if "attn" in n else 0.0)})
+             for n, g, t, _ in ds + copies]
+    _write(str(tmp_path / "fetch" / "run_counter_collection.csv"), fetch)
+    _write(str(tmp_path / "write" / "run_counter_collection.csv"), write)
+    ps.attn(str(tmp_path), "llama7b_p512", "CMD", "F", "W")
     md = (tmp_path / "attn_counters_llama7b_p512.md").read_text()
     row = next(line for line in md.splitlines() if line.startswith("| `tree_attn_shared`"))
     cells = [c.strip() for c in row.split("|")[1:-1]]
@@ -117,3 +124,6 @@ def test_attention_mix_per_64_mfma(tmp_path, monkeypatch):
     assert cells[8] == "150" and cells[9] == "60.0" and cells[10] == "0.100"
     wrow = next(line for line in md.splitlines() if line.startswith("| `tree_attn_window`"))
     assert wrow.split("|")[9].strip() == "–"
+    # bytes: 2048 KiB fetched x 2 (the copies' factor) = 4.19 MB, 512 KiB written = 0.52 MB
+    brow = [line for line in md.splitlines() if line.startswith("| `tree_attn_shared`")][1]
+    assert [c.strip() for c in brow.split("|")[3:5]] == ["4.19", "0.52"]
